@@ -1,0 +1,184 @@
+/*
+ * pic_attn.h -- position-free paged attention on MI355X (gfx950).
+ *
+ * C ABI of libpic_attn.so.  The operation is the attention step of a KV cache
+ * that stores keys without positional rotation (MiniPIC, Sec. 3.2.1 "Mechanism"):
+ * RoPE is applied inside the kernel to the queries and to every K tile at the
+ * token's per-request logical position, and the visible keys of each query follow
+ * the span structure that the SSep / PDep primitives and block-aligned padding
+ * define (Sec. 3.1.1, eq. (1)).  The score of query t and cached key j is
+ *     (R_{p(t)} q_t)^T (R_{p(j)} k~_j) * scale
+ * where k~ is the stored (unrotated) key and p(.) the request's logical position.
+ *
+ * Conventions shared by every entry point
+ *  - Every call returns a pic_status.  Arguments are validated on the host before
+ *    anything is enqueued; on an error nothing is launched and pic_last_error()
+ *    returns a message (thread-local, valid until the next call on that thread).
+ *  - Device contents (block ids, positions, slot numbers) are trusted, as the
+ *    paper keeps validation outside the engine (Sec. 3.1.2).  Out-of-range block
+ *    ids or slots are undefined behaviour.
+ *  - "DEVICE" pointers are HIP device memory; "HOST" pointers are host memory read
+ *    during the call only.  All buffers are owned by the caller; the library
+ *    allocates nothing and keeps no state between calls.
+ *  - Work is enqueued asynchronously on `stream` (a hipStream_t, or NULL for the
+ *    null stream).  Kernel execution errors surface at the caller's next sync.
+ *  - Tensors are dense and row-major in the shapes given.  Q, O, the K/V pools
+ *    and new K/V rows share cfg->dtype.
+ */
+#ifndef PIC_ATTN_H
+#define PIC_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t pic_status;
+#define PIC_OK 0
+#define PIC_EINVAL 1       /* malformed argument (null pointer, bad shape, bad span list) */
+#define PIC_EUNSUPPORTED 2 /* well formed but not implemented (e.g. head_dim 96) */
+#define PIC_EHIP 3         /* a HIP runtime call or launch failed */
+#define PIC_EWORKSPACE 4   /* workspace smaller than pic_workspace_size() asked for */
+
+/* element types (cfg->dtype) */
+#define PIC_BF16 0
+#define PIC_F32 1
+
+/* RoPE pairing (cfg->rope_style).  The paper uses the model's rotary embedding
+ * (Sec. 3.2.1) without naming a pairing; NeoX (element i with i + D/2, the
+ * Llama convention) is the default, GPT-J (2i with 2i+1) the alternative. */
+#define PIC_ROPE_NEOX 0
+#define PIC_ROPE_GPTJ 1
+
+/* span flags (span_flags[]), Sec. 3.1.1:
+ *  PIC_SSEP  the span is detached from what precedes it: it sees only itself;
+ *  PIC_PDEP  the span depends on the whole preceding prompt: it sees everything;
+ *  neither   the span continues the previous span's hash chain and keeps its window;
+ *  PIC_QUERY the span's tokens are computed in this prefill call (they are the
+ *            query rows of q and o). */
+#define PIC_SSEP 1
+#define PIC_PDEP 2
+#define PIC_QUERY 4
+
+typedef struct pic_config {
+    int32_t num_q_heads;   /* Hq > 0 */
+    int32_t num_kv_heads;  /* Hkv > 0, Hq % Hkv == 0; query head h reads KV head h / (Hq/Hkv) */
+    int32_t head_dim;      /* D: 64 or 128 */
+    int32_t block_size;    /* tokens per KV block: must be 16 */
+    int32_t dtype;         /* PIC_BF16 or PIC_F32 */
+    int32_t rope_style;    /* PIC_ROPE_NEOX or PIC_ROPE_GPTJ */
+    double rope_theta;     /* base of omega_i = theta^(-2i/D), > 0 */
+    float softmax_scale;   /* 0 means 1/sqrt(D) (Sec. 3.2.1 score equation) */
+    int32_t k_prerotated;  /* 0: the pool holds unrotated K and q is unrotated (the method);
+                              1: both are already rotated and no RoPE is applied (the
+                                 baseline FlashAttention of Sec. 3.2.2, for comparison) */
+} pic_config;
+
+/* Span structure of a batch (HOST).  Request r has seq_lens[r] >= 1 tokens
+ * (cached and new) indexed n = 0..L_r-1 and spans cu_spans[r] .. cu_spans[r+1]-1
+ * (at least one).  span_start[] is 0 for a request's first span and strictly
+ * increasing.  span_window, if not NULL, holds an explicit window start per span
+ * (-1: use the flags), with 0 <= w <= span start; it generalises SSep/PDep. */
+typedef struct pic_batch_host {
+    int32_t num_reqs;
+    const int32_t* seq_lens;    /* HOST [R] */
+    const int32_t* cu_spans;    /* HOST [R+1], cu_spans[0] == 0 */
+    const int32_t* span_start;  /* HOST [S] */
+    const int32_t* span_flags;  /* HOST [S] */
+    const int32_t* span_window; /* HOST [S] or NULL */
+} pic_batch_host;
+
+/* Per-token metadata (DEVICE).  Token n of request r lives in physical block
+ * block_tables[r*max_blocks + n/16] at offset n%16; its logical position (only fed
+ * to RoPE, never to the mask) is positions[sum_{r'<r} L_r' + n].  A physical block
+ * may appear in many requests and more than once in one request. */
+typedef struct pic_batch_dev {
+    const int32_t* block_tables; /* DEVICE [R][max_blocks] */
+    int32_t max_blocks;          /* >= ceil(L_r / 16) for every r */
+    const int32_t* positions;    /* DEVICE [sum L_r], any int32 values */
+} pic_batch_dev;
+
+/* Optional cos/sin table (the paper's cos_sin lookup, Sec. 3.2.2): entry
+ * [p][i] = (cos(p*omega_i), sin(p*omega_i)) as two float32, for p in [0, len).
+ * Built by pic_rope_table_build.  Positions outside [0, len), and every position
+ * when data is NULL, are rotated with cos/sin computed in the kernel from an exact
+ * fixed-point phase. */
+typedef struct pic_rope_table {
+    const void* data; /* DEVICE [len][D/2][2] float32, or NULL */
+    int32_t len;
+} pic_rope_table;
+
+/* Library version (major*10000 + minor*100 + patch). */
+int32_t pic_version(void);
+
+/* Message of the last error on this thread ("" if none). */
+const char* pic_last_error(void);
+
+/* Bytes of the cos/sin table for positions [0, num_positions). */
+pic_status pic_rope_table_bytes(const pic_config* cfg, int32_t num_positions, size_t* bytes);
+
+/* Fill `table` (DEVICE, pic_rope_table_bytes bytes) with cos/sin of p*omega_i for
+ * p in [0, num_positions), computed in float64 and rounded to float32. */
+pic_status pic_rope_table_build(const pic_config* cfg, int32_t num_positions, void* table, void* stream);
+
+/* Rotate x (DEVICE [n][num_heads][D], cfg->dtype) in place by R_p with
+ * p = positions[i] (DEVICE [n]) for row i.  This is the conventional
+ * rotary-embedding step; it builds the pre-rotated inputs of the
+ * k_prerotated = 1 comparison path. */
+pic_status pic_rope_rotate(const pic_config* cfg, const pic_rope_table* rope, void* x, int32_t n,
+                           int32_t num_heads, const int32_t* positions, void* stream);
+
+/* Store new key/value rows in the paged pool (Sec. 3.2.1: keys are cached
+ * unrotated).  Row i of k_new/v_new (DEVICE [n][Hkv][D]) goes to slot
+ * s = slot_mapping[i] (DEVICE [n]): pool[s/16][h][s%16][:] for every KV head h,
+ * pools being DEVICE [num_blocks][Hkv][16][D].  Negative slots are skipped.
+ * Slots must be distinct (a repeated slot is a race).  Bit-exact copy. */
+pic_status pic_kv_write(const pic_config* cfg, void* k_pool, void* v_pool, int32_t num_blocks,
+                        const void* k_new, const void* v_new, const int32_t* slot_mapping, int32_t n,
+                        void* stream);
+
+/* Workspace bytes that pic_attn_prefill (is_decode = 0) or pic_attn_decode
+ * (is_decode = 1) needs for this configuration and batch (split-KV partial
+ * results).  May be 0. */
+pic_status pic_workspace_size(const pic_config* cfg, const pic_batch_host* batch, int32_t is_decode,
+                              size_t* bytes);
+
+/* Prefill attention for the tokens of every PIC_QUERY span.
+ *  q  DEVICE [total_q][Hq][D]: one row per query token, request-major, spans and
+ *     tokens in sequence order; unrotated unless cfg->k_prerotated.
+ *  o  DEVICE [total_q][Hq][D], same order; fully overwritten.
+ *  k_pool, v_pool DEVICE [num_blocks][Hkv][16][D] holding every token of every
+ *     request (write the call's fresh rows with pic_kv_write first, on the same
+ *     stream).
+ * Query token t of request r (sequence index n_t) attends to keys j with
+ * w(n_t) <= j <= n_t, w being the window start of its span: the span start for
+ * PIC_SSEP, 0 for PIC_PDEP, the previous span's window otherwise (0 for the first
+ * span).  Keys outside every window are never read. */
+pic_status pic_attn_prefill(const pic_config* cfg, const pic_batch_host* batch, const pic_batch_dev* dev,
+                            const pic_rope_table* rope, const void* q, void* o, const void* k_pool,
+                            const void* v_pool, int32_t num_blocks, void* workspace, size_t workspace_bytes,
+                            void* stream);
+
+/* Decode attention: one query per request, the request's last token n = L_r - 1
+ * (already stored with pic_kv_write), with the window of the span holding it.
+ *  q, o DEVICE [R][Hq][D]. */
+pic_status pic_attn_decode(const pic_config* cfg, const pic_batch_host* batch, const pic_batch_dev* dev,
+                           const pic_rope_table* rope, const void* q, void* o, const void* k_pool,
+                           const void* v_pool, int32_t num_blocks, void* workspace, size_t workspace_bytes,
+                           void* stream);
+
+/* Test hook: the work decomposition the prefill/decode call would launch, as
+ * rows of 8 int32 {request, kv_head, first query row (flattened token*G+head
+ * offset within the span), end query row, key begin, key end, span first token,
+ * partial slot or -1}.  Writes min(*n_items, capacity) rows to `items` (HOST)
+ * and the full count to *n_items.  No HIP call is made. */
+pic_status pic_plan_debug(const pic_config* cfg, const pic_batch_host* batch, int32_t is_decode,
+                          int32_t* items, int32_t capacity, int32_t* n_items);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PIC_ATTN_H */

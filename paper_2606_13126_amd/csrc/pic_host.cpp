@@ -1,0 +1,410 @@
+// Host side of libpic_attn: argument validation, the work planner and the
+// C-ABI entry points declared in include/pic_attn.h.
+//
+// The planner turns the host span descriptor into launch groups: one group per
+// PIC_QUERY span (prefill) or per request (decode), each with its window start
+// (Sec. 3.1.1: SSEP -> span start, PDEP -> 0, unflagged -> previous span's
+// window), its row tiles and its key splits.  Groups travel to the kernels by
+// value as a kernel argument, so a call enqueues no host-to-device copy.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/pic_attn.h"
+#include "pic_internal.h"
+
+namespace {
+
+thread_local std::string g_error;
+
+pic_status fail(pic_status st, const std::string& msg) {
+    g_error = msg;
+    return st;
+}
+
+pic_status check_config(const pic_config* c) {
+    if (c == nullptr) return fail(PIC_EINVAL, "cfg is NULL");
+    if (c->num_q_heads <= 0 || c->num_kv_heads <= 0) return fail(PIC_EINVAL, "head counts must be positive");
+    if (c->num_q_heads % c->num_kv_heads != 0) return fail(PIC_EINVAL, "num_q_heads must be a multiple of num_kv_heads");
+    if (c->block_size != pic::kBlock) return fail(PIC_EUNSUPPORTED, "block_size must be 16");
+    if (c->head_dim != 64 && c->head_dim != 128) return fail(PIC_EUNSUPPORTED, "head_dim must be 64 or 128");
+    if (c->dtype != PIC_BF16 && c->dtype != PIC_F32) return fail(PIC_EUNSUPPORTED, "dtype must be PIC_BF16 or PIC_F32");
+    if (c->rope_style != PIC_ROPE_NEOX && c->rope_style != PIC_ROPE_GPTJ) return fail(PIC_EINVAL, "unknown rope_style");
+    if (!(c->rope_theta > 0.0) || !std::isfinite(c->rope_theta)) return fail(PIC_EINVAL, "rope_theta must be positive");
+    if (!(c->softmax_scale >= 0.f) || !std::isfinite(c->softmax_scale)) return fail(PIC_EINVAL, "softmax_scale must be >= 0");
+    if (c->k_prerotated != 0 && c->k_prerotated != 1) return fail(PIC_EINVAL, "k_prerotated must be 0 or 1");
+    return PIC_OK;
+}
+
+// Window start of every span of request r (the rule of the span flags, or the
+// explicit override).
+pic_status span_windows(const pic_batch_host* b, int r, std::vector<int32_t>& w) {
+    const int s0 = b->cu_spans[r], s1 = b->cu_spans[r + 1];
+    w.assign(s1 - s0, 0);
+    int32_t prev = 0;
+    for (int k = s0; k < s1; ++k) {
+        const int32_t f = b->span_flags[k];
+        int32_t wk;
+        if (b->span_window != nullptr && b->span_window[k] >= 0)
+            wk = b->span_window[k];
+        else if (f & PIC_SSEP)
+            wk = b->span_start[k];
+        else if (f & PIC_PDEP)
+            wk = 0;
+        else
+            wk = prev;
+        w[k - s0] = wk;
+        prev = wk;
+    }
+    return PIC_OK;
+}
+
+pic_status check_batch(const pic_batch_host* b) {
+    if (b == nullptr) return fail(PIC_EINVAL, "batch is NULL");
+    if (b->num_reqs < 0) return fail(PIC_EINVAL, "num_reqs < 0");
+    if (b->num_reqs == 0) return PIC_OK;
+    if (!b->seq_lens || !b->cu_spans || !b->span_start || !b->span_flags)
+        return fail(PIC_EINVAL, "batch arrays must not be NULL");
+    if (b->cu_spans[0] != 0) return fail(PIC_EINVAL, "cu_spans[0] must be 0");
+    int64_t total = 0;
+    for (int r = 0; r < b->num_reqs; ++r) {
+        const int32_t L = b->seq_lens[r];
+        if (L < 1) return fail(PIC_EINVAL, "seq_lens[" + std::to_string(r) + "] must be >= 1");
+        total += L;
+        const int s0 = b->cu_spans[r], s1 = b->cu_spans[r + 1];
+        if (s1 <= s0) return fail(PIC_EINVAL, "request " + std::to_string(r) + " has no span");
+        if (b->span_start[s0] != 0) return fail(PIC_EINVAL, "first span of a request must start at 0");
+        for (int k = s0; k < s1; ++k) {
+            const int32_t f = b->span_flags[k];
+            if (f & ~(PIC_SSEP | PIC_PDEP | PIC_QUERY)) return fail(PIC_EINVAL, "unknown span flag bits");
+            if ((f & PIC_SSEP) && (f & PIC_PDEP)) return fail(PIC_EINVAL, "a span cannot be both SSEP and PDEP");
+            if (b->span_start[k] < 0 || b->span_start[k] >= L) return fail(PIC_EINVAL, "span_start out of range");
+            if (k > s0 && b->span_start[k] <= b->span_start[k - 1])
+                return fail(PIC_EINVAL, "span_start must be strictly increasing within a request");
+            if (b->span_window != nullptr && b->span_window[k] >= 0 && b->span_window[k] > b->span_start[k])
+                return fail(PIC_EINVAL, "span_window must not exceed the span start");
+        }
+    }
+    if (total > INT32_MAX) return fail(PIC_EINVAL, "total tokens exceed int32");
+    return PIC_OK;
+}
+
+struct HostPlan {
+    std::vector<pic::Group> groups;
+    int64_t n_parts = 0;
+};
+
+int32_t round_up(int64_t x, int64_t m) { return (int32_t)((x + m - 1) / m * m); }
+
+// Groups, their split policy and bases.  f32 groups hold one item per
+// (query token, query head); bf16 groups hold (row tile, KV head, split) items.
+pic_status make_plan(const pic_config* c, const pic_batch_host* b, bool decode, HostPlan& hp) {
+    hp.groups.clear();
+    hp.n_parts = 0;
+    const int G = c->num_q_heads / c->num_kv_heads;
+    std::vector<int32_t> w;
+    int64_t pos_off = 0, q_row = 0;
+    for (int r = 0; r < b->num_reqs; ++r) {
+        span_windows(b, r, w);
+        const int s0 = b->cu_spans[r], s1 = b->cu_spans[r + 1];
+        const int32_t L = b->seq_lens[r];
+        if (decode) {
+            pic::Group g{};
+            g.req = r;
+            g.tok0 = L - 1;
+            g.n_tok = 1;
+            g.q_row0 = r;
+            g.win = w[s1 - s0 - 1];
+            g.pos_off = (int32_t)pos_off;
+            hp.groups.push_back(g);
+        } else {
+            for (int k = s0; k < s1; ++k) {
+                if (!(b->span_flags[k] & PIC_QUERY)) continue;
+                const int32_t e = k + 1 < s1 ? b->span_start[k + 1] : L;
+                pic::Group g{};
+                g.req = r;
+                g.tok0 = b->span_start[k];
+                g.n_tok = e - g.tok0;
+                g.q_row0 = (int32_t)q_row;
+                g.win = w[k - s0];
+                g.pos_off = (int32_t)pos_off;
+                q_row += g.n_tok;
+                hp.groups.push_back(g);
+            }
+        }
+        pos_off += L;
+    }
+    if (q_row > INT32_MAX / 2) return fail(PIC_EINVAL, "too many query rows");
+
+    if (c->dtype == PIC_F32) {
+        for (auto& g : hp.groups) {
+            g.n_rt = g.n_tok;
+            g.n_split = 1;
+            g.split_keys = 0;
+        }
+    } else {
+        // split keys only when the unsplit items cannot fill the chip
+        int64_t base = 0, work = 0;
+        for (auto& g : hp.groups) {
+            g.n_rt = (int32_t)(((int64_t)g.n_tok * G + pic::kTileRows - 1) / pic::kTileRows);
+            const int64_t keys = (int64_t)g.tok0 + g.n_tok - g.win;
+            base += (int64_t)g.n_rt * c->num_kv_heads;
+            work += (int64_t)g.n_rt * c->num_kv_heads * keys;
+        }
+        int64_t chunk = INT32_MAX;
+        if (base < pic::kTargetCUs && work > 0)
+            chunk = std::max<int64_t>(4 * pic::kTileKeys, round_up((work + pic::kTargetCUs - 1) / pic::kTargetCUs,
+                                                                   pic::kTileKeys));
+        for (auto& g : hp.groups) {
+            const int64_t keys = (int64_t)g.tok0 + g.n_tok - g.win;
+            if (keys <= chunk) {
+                g.n_split = 1;
+                g.split_keys = round_up(keys, pic::kTileKeys);
+            } else {
+                g.n_split = (int32_t)((keys + chunk - 1) / chunk);
+                g.split_keys = (int32_t)chunk;
+            }
+        }
+        // heaviest items first
+        std::stable_sort(hp.groups.begin(), hp.groups.end(), [](const pic::Group& x, const pic::Group& y) {
+            const int64_t cx = (int64_t)std::min(x.n_tok, pic::kTileRows) * std::min<int64_t>(x.split_keys, x.tok0 + x.n_tok - x.win);
+            const int64_t cy = (int64_t)std::min(y.n_tok, pic::kTileRows) * std::min<int64_t>(y.split_keys, y.tok0 + y.n_tok - y.win);
+            return cx > cy;
+        });
+    }
+    return PIC_OK;
+}
+
+int64_t items_of(const pic_config* c, const pic::Group& g) {
+    if (c->dtype == PIC_F32) return (int64_t)g.n_tok * c->num_q_heads;
+    return (int64_t)g.n_rt * c->num_kv_heads * g.n_split;
+}
+
+// Cut the group list into launches of at most kMaxGroups groups and assign bases.
+void make_launches(const pic_config* c, HostPlan& hp, std::vector<pic::Plan>& launches) {
+    launches.clear();
+    int64_t part = 0;
+    size_t i = 0;
+    while (i < hp.groups.size()) {
+        pic::Plan p;
+        std::memset(&p, 0, sizeof(p));
+        int64_t item = 0, merge = 0;
+        while (i < hp.groups.size() && p.n_groups < pic::kMaxGroups) {
+            pic::Group g = hp.groups[i];
+            const int64_t n = items_of(c, g);
+            if (item + round_up(n, 8) > INT32_MAX / 2 && p.n_groups > 0) break;
+            g.item_base = (int32_t)item;
+            item += round_up(n, 8);
+            if (c->dtype != PIC_F32 && g.n_split > 1) {
+                g.part_base = (int32_t)part;
+                part += (int64_t)g.n_rt * c->num_kv_heads * g.n_split;
+                g.merge_base = (int32_t)merge;
+                merge += (int64_t)g.n_rt * c->num_kv_heads;
+            }
+            p.g[p.n_groups++] = g;
+            ++i;
+        }
+        p.n_items = (int32_t)item;
+        p.n_merge = (int32_t)merge;
+        launches.push_back(p);
+    }
+    hp.n_parts = part;
+}
+
+size_t workspace_bytes(const pic_config* c, int64_t n_parts) {
+    return (size_t)n_parts * pic::kTileRows * ((size_t)c->head_dim + 2) * sizeof(float);
+}
+
+pic_status hip_status(int e, const char* what) {
+    if (e != hipSuccess) return fail(PIC_EHIP, std::string(what) + ": " + hipGetErrorString((hipError_t)e));
+    return PIC_OK;
+}
+
+pic_status run_attention(const pic_config* c, const pic_batch_host* b, const pic_batch_dev* dv,
+                         const pic_rope_table* rope, const void* q, void* o, const void* k_pool, const void* v_pool,
+                         int32_t num_blocks, void* ws, size_t ws_bytes, void* stream, bool decode) {
+    pic_status st = check_config(c);
+    if (st) return st;
+    if ((st = check_batch(b))) return st;
+    if (b->num_reqs == 0) return PIC_OK;
+    if (dv == nullptr || dv->block_tables == nullptr || dv->positions == nullptr)
+        return fail(PIC_EINVAL, "device batch arrays must not be NULL");
+    if (num_blocks <= 0) return fail(PIC_EINVAL, "num_blocks must be positive");
+    for (int r = 0; r < b->num_reqs; ++r)
+        if ((int64_t)dv->max_blocks * pic::kBlock < b->seq_lens[r])
+            return fail(PIC_EINVAL, "max_blocks too small for seq_lens[" + std::to_string(r) + "]");
+    if (!k_pool || !v_pool) return fail(PIC_EINVAL, "pools must not be NULL");
+    if (rope != nullptr && rope->data != nullptr && rope->len < 0) return fail(PIC_EINVAL, "rope table len < 0");
+
+    HostPlan hp;
+    if ((st = make_plan(c, b, decode, hp))) return st;
+    int64_t rows = 0;
+    for (auto& g : hp.groups) rows += g.n_tok;
+    if (rows == 0) return PIC_OK;
+    if (!q || !o) return fail(PIC_EINVAL, "q and o must not be NULL");
+    std::vector<pic::Plan> launches;
+    make_launches(c, hp, launches);
+    const size_t need = workspace_bytes(c, hp.n_parts);
+    if (need > 0 && (ws == nullptr || ws_bytes < need))
+        return fail(PIC_EWORKSPACE, "workspace needs " + std::to_string(need) + " bytes");
+
+    pic::Args a{};
+    a.q = q;
+    a.o = o;
+    a.k_pool = k_pool;
+    a.v_pool = v_pool;
+    a.block_tables = dv->block_tables;
+    a.positions = dv->positions;
+    const bool table = rope != nullptr && rope->data != nullptr && rope->len > 0;
+    a.rope_table = table ? static_cast<const float*>(rope->data) : nullptr;
+    a.rope_len = table ? rope->len : 0;
+    a.part_o = static_cast<float*>(ws);
+    a.part_ml = hp.n_parts ? static_cast<float*>(ws) + (size_t)hp.n_parts * pic::kTileRows * c->head_dim : nullptr;
+    a.theta = c->rope_theta;
+    const double scale = c->softmax_scale > 0.f ? (double)c->softmax_scale : 1.0 / std::sqrt((double)c->head_dim);
+    a.scale_log2 = (float)(scale * 1.4426950408889634);
+    a.max_blocks = dv->max_blocks;
+    a.hq = c->num_q_heads;
+    a.hkv = c->num_kv_heads;
+    a.group = c->num_q_heads / c->num_kv_heads;
+    for (const auto& p : launches) {
+        const int e = pic::launch_attention(c->dtype, c->rope_style, c->head_dim, c->k_prerotated == 0, p, a, stream);
+        if ((st = hip_status(e, "attention launch"))) return st;
+    }
+    return PIC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t pic_version(void) { return 100; }
+
+const char* pic_last_error(void) { return g_error.c_str(); }
+
+pic_status pic_rope_table_bytes(const pic_config* cfg, int32_t num_positions, size_t* bytes) {
+    pic_status st = check_config(cfg);
+    if (st) return st;
+    if (num_positions < 0 || bytes == nullptr) return fail(PIC_EINVAL, "bad num_positions or bytes pointer");
+    *bytes = (size_t)num_positions * (cfg->head_dim / 2) * 2 * sizeof(float);
+    return PIC_OK;
+}
+
+pic_status pic_rope_table_build(const pic_config* cfg, int32_t num_positions, void* table, void* stream) {
+    pic_status st = check_config(cfg);
+    if (st) return st;
+    if (num_positions < 0) return fail(PIC_EINVAL, "num_positions < 0");
+    if (num_positions > 0 && table == nullptr) return fail(PIC_EINVAL, "table is NULL");
+    return hip_status(pic::launch_rope_table(cfg->head_dim, cfg->rope_theta, num_positions,
+                                             static_cast<float*>(table), stream),
+                      "rope table launch");
+}
+
+pic_status pic_rope_rotate(const pic_config* cfg, const pic_rope_table* rope, void* x, int32_t n, int32_t num_heads,
+                           const int32_t* positions, void* stream) {
+    pic_status st = check_config(cfg);
+    if (st) return st;
+    if (n < 0 || num_heads <= 0) return fail(PIC_EINVAL, "bad n or num_heads");
+    if (n == 0) return PIC_OK;
+    if (x == nullptr || positions == nullptr) return fail(PIC_EINVAL, "x and positions must not be NULL");
+    const bool table = rope != nullptr && rope->data != nullptr && rope->len > 0;
+    return hip_status(pic::launch_rope_rotate(cfg->dtype, cfg->rope_style, cfg->head_dim, cfg->rope_theta,
+                                              table ? static_cast<const float*>(rope->data) : nullptr,
+                                              table ? rope->len : 0, x, n, num_heads, positions, stream),
+                      "rope rotate launch");
+}
+
+pic_status pic_kv_write(const pic_config* cfg, void* k_pool, void* v_pool, int32_t num_blocks, const void* k_new,
+                        const void* v_new, const int32_t* slot_mapping, int32_t n, void* stream) {
+    pic_status st = check_config(cfg);
+    if (st) return st;
+    if (n < 0 || num_blocks < 0) return fail(PIC_EINVAL, "n and num_blocks must be >= 0");
+    if (n == 0) return PIC_OK;
+    if (!k_pool || !v_pool || !k_new || !v_new || !slot_mapping) return fail(PIC_EINVAL, "NULL buffer");
+    if (num_blocks == 0) return fail(PIC_EINVAL, "empty pool");
+    return hip_status(pic::launch_kv_write(cfg->dtype, cfg->num_kv_heads, cfg->head_dim, k_pool, v_pool, k_new, v_new,
+                                           slot_mapping, n, stream),
+                      "kv_write launch");
+}
+
+pic_status pic_workspace_size(const pic_config* cfg, const pic_batch_host* batch, int32_t is_decode, size_t* bytes) {
+    pic_status st = check_config(cfg);
+    if (st) return st;
+    if ((st = check_batch(batch))) return st;
+    if (bytes == nullptr) return fail(PIC_EINVAL, "bytes is NULL");
+    HostPlan hp;
+    if ((st = make_plan(cfg, batch, is_decode != 0, hp))) return st;
+    std::vector<pic::Plan> launches;
+    make_launches(cfg, hp, launches);
+    *bytes = workspace_bytes(cfg, hp.n_parts);
+    return PIC_OK;
+}
+
+pic_status pic_attn_prefill(const pic_config* cfg, const pic_batch_host* batch, const pic_batch_dev* dev,
+                            const pic_rope_table* rope, const void* q, void* o, const void* k_pool, const void* v_pool,
+                            int32_t num_blocks, void* workspace, size_t workspace_bytes, void* stream) {
+    return run_attention(cfg, batch, dev, rope, q, o, k_pool, v_pool, num_blocks, workspace, workspace_bytes, stream,
+                         false);
+}
+
+pic_status pic_attn_decode(const pic_config* cfg, const pic_batch_host* batch, const pic_batch_dev* dev,
+                           const pic_rope_table* rope, const void* q, void* o, const void* k_pool, const void* v_pool,
+                           int32_t num_blocks, void* workspace, size_t workspace_bytes, void* stream) {
+    return run_attention(cfg, batch, dev, rope, q, o, k_pool, v_pool, num_blocks, workspace, workspace_bytes, stream,
+                         true);
+}
+
+pic_status pic_plan_debug(const pic_config* cfg, const pic_batch_host* batch, int32_t is_decode, int32_t* items,
+                          int32_t capacity, int32_t* n_items) {
+    pic_status st = check_config(cfg);
+    if (st) return st;
+    if ((st = check_batch(batch))) return st;
+    if (n_items == nullptr || capacity < 0 || (capacity > 0 && items == nullptr))
+        return fail(PIC_EINVAL, "bad output arguments");
+    HostPlan hp;
+    if ((st = make_plan(cfg, batch, is_decode != 0, hp))) return st;
+    std::vector<pic::Plan> launches;
+    make_launches(cfg, hp, launches);
+    const int G = cfg->num_q_heads / cfg->num_kv_heads;
+    int64_t n = 0;
+    auto emit = [&](int32_t r, int32_t h, int32_t rl, int32_t rh, int32_t kl, int32_t kh, int32_t t0, int32_t slot) {
+        if (n < capacity) {
+            int32_t* it = items + n * 8;
+            it[0] = r; it[1] = h; it[2] = rl; it[3] = rh; it[4] = kl; it[5] = kh; it[6] = t0; it[7] = slot;
+        }
+        ++n;
+    };
+    for (const auto& p : launches)
+        for (int gi = 0; gi < p.n_groups; ++gi) {
+            const pic::Group& g = p.g[gi];
+            if (cfg->dtype == PIC_F32) {
+                for (int t = 0; t < g.n_tok; ++t)
+                    for (int h = 0; h < cfg->num_q_heads; ++h) {
+                        const int32_t row = t * G + h % G;
+                        emit(g.req, h / G, row, row + 1, g.win, g.tok0 + t + 1, g.tok0, -1);
+                    }
+                continue;
+            }
+            for (int kvh = 0; kvh < cfg->num_kv_heads; ++kvh)
+                for (int s = 0; s < g.n_split; ++s)
+                    for (int rt = 0; rt < g.n_rt; ++rt) {
+                        const int32_t rl = rt * pic::kTileRows;
+                        const int32_t rh = std::min(rl + pic::kTileRows, g.n_tok * G);
+                        const int32_t t_last = g.tok0 + (rh - 1) / G;
+                        const int32_t kl = g.win + s * g.split_keys;
+                        const int32_t kh = std::min(kl + g.split_keys, t_last + 1);
+                        if (kl >= kh) continue;
+                        const int32_t slot =
+                            g.n_split > 1 ? g.part_base + (kvh * g.n_split + s) * g.n_rt + rt : -1;
+                        emit(g.req, kvh, rl, rh, kl, kh, g.tok0, slot);
+                    }
+        }
+    *n_items = (int32_t)std::min<int64_t>(n, INT32_MAX);
+    return PIC_OK;
+}
+
+}  // extern "C"

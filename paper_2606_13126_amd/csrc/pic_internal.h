@@ -1,0 +1,69 @@
+// Internal types shared by the host planner (pic_host.cpp) and the HIP kernels
+// (pic_kernels.hip).  Not part of the public ABI.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+namespace pic {
+
+constexpr int kBlock = 16;        // tokens per KV block
+constexpr int kTileRows = 256;    // query rows (token x head-in-group) per prefill workgroup
+constexpr int kTileKeys = 64;     // keys per K/V tile of the prefill kernel
+constexpr int kMaxGroups = 64;    // groups passed by value in one launch
+constexpr int kTargetCUs = 256;   // MI355X compute units the split policy fills
+
+// One query span of one request (prefill) or one request's last token (decode).
+// Its work items are (row tile, KV head, key split) triples, enumerated from
+// item_base; partial results of split items live at part_base onwards.
+struct Group {
+    int32_t req;         // request index (row of the block table)
+    int32_t tok0;        // sequence index of the span's first query token
+    int32_t n_tok;       // query tokens in the span
+    int32_t q_row0;      // row of tok0 in q / o
+    int32_t win;         // window start of the span's tokens
+    int32_t pos_off;     // offset of the request's token 0 in `positions`
+    int32_t n_rt;        // row tiles (ceil(n_tok * G / kTileRows))
+    int32_t n_split;     // key splits per (row tile, KV head)
+    int32_t split_keys;  // keys per split (a multiple of kTileKeys)
+    int32_t item_base;   // first item (block index) of the group; a multiple of 8
+    int32_t part_base;   // first partial slot (n_split > 1)
+    int32_t merge_base;  // first merge block (n_split > 1)
+};
+
+struct Plan {
+    int32_t n_groups;
+    int32_t n_items;     // blocks of the attention launch
+    int32_t n_merge;     // blocks of the merge launch
+    int32_t pad_;
+    Group g[kMaxGroups];
+};
+
+struct Args {
+    const void* q;
+    void* o;
+    const void* k_pool;
+    const void* v_pool;
+    const int32_t* block_tables;
+    const int32_t* positions;
+    const float* rope_table;  // [rope_len][D/2][2] or null
+    float* part_o;            // [slot][kTileRows][D] unnormalised partial outputs
+    float* part_ml;           // [slot][kTileRows][2] running max (log2 units) and sum
+    double theta;
+    float scale_log2;         // softmax scale * log2(e)
+    int32_t max_blocks;
+    int32_t rope_len;
+    int32_t hq;
+    int32_t hkv;
+    int32_t group;            // G = hq / hkv
+};
+
+// Launchers implemented in pic_kernels.hip.  Each returns a hipError_t value.
+int launch_kv_write(int dtype, int hkv, int d, void* k_pool, void* v_pool, const void* k_new,
+                    const void* v_new, const int32_t* slots, int n, void* stream);
+int launch_rope_table(int d, double theta, int n_pos, float* table, void* stream);
+int launch_rope_rotate(int dtype, int style, int d, double theta, const float* table, int rope_len, void* x,
+                       int n, int heads, const int32_t* positions, void* stream);
+int launch_attention(int dtype, int style, int d, bool rope, const Plan& plan, const Args& args, void* stream);
+
+}  // namespace pic

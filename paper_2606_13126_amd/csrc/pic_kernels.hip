@@ -1,0 +1,729 @@
+// HIP kernels of libpic_attn for MI355X (gfx950, CDNA4).
+//
+//  * kv_write      scatter of unrotated K/V rows into the paged pool (Sec. 3.2.1:
+//                  the cache keeps keys without positional rotation).
+//  * rope_table    the cos/sin lookup table of Sec. 3.2.2, built in float64.
+//  * rope_rotate   conventional in-place rotary embedding (comparison path only).
+//  * prefill_bf16  paged flash attention, bf16 MFMA (v_mfma_f32_32x32x16_bf16) for
+//                  S^T = K Q^T and O^T = V^T P^T, RoPE fused into the K-tile load
+//                  (Sec. 3.2.2: load tile, look up cos/sin at the tile's positions,
+//                  rotate, then the dot products), exp2 online softmax, window mask
+//                  of Sec. 3.1.1 with whole-block skipping, optional key splits.
+//  * merge         combines key-split partial results (log-sum-exp merge).
+//  * attn_f32      fp32 VALU flash attention for the float32 path.
+//
+// Layouts: pools [num_blocks][Hkv][16][D]; q/o [rows][Hq][D]; positions int32 per
+// token, request-major.  One workgroup of the bf16 kernel owns up to 256 query rows
+// (token x query head of one KV head's group) and one key range.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "pic_internal.h"
+
+namespace pic {
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+
+constexpr int kNeox = 0;
+constexpr float kNegBig = -1.0e30f;  // finite "minus infinity" for running maxima
+constexpr double kInv2Pi = 0.15915494309189533577;
+
+__device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// Round two floats to bf16 (round to nearest even) and pack them, lo first.
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    bf16x2_t v = {(__bf16)lo, (__bf16)hi};
+    return __builtin_bit_cast(uint32_t, v);
+}
+
+// ---------------------------------------------------------------------------------
+// RoPE angles.  Pair i turns by p * omega_i with omega_i = theta^(-2i/D).  The angle
+// is kept as a 64-bit binary fraction of a revolution, F_i = frac(omega_i / 2pi)
+// scaled by 2^64, so p * F_i (mod 2^64) is the exact phase of any int32 position
+// (negative ones included) up to the rounding of F_i; sin/cos then only see a
+// reduced argument in [-0.5, 0.5) revolutions.
+// ---------------------------------------------------------------------------------
+__device__ uint64_t rope_phase_step(double theta, int i, int d) {
+    double rev = pow(theta, -2.0 * (double)i / (double)d) * kInv2Pi;
+    rev -= floor(rev);
+    return (uint64_t)(rev * 18446744073709551616.0);
+}
+
+__device__ __forceinline__ void rope_cs(int32_t pos, uint64_t step, float& c, float& s) {
+    const uint64_t ph = (uint64_t)(int64_t)pos * step;
+    const float r = (float)(int32_t)(ph >> 32) * 0x1p-32f;
+    sincospif(2.0f * r, &s, &c);
+}
+
+__device__ __forceinline__ void rope_cs_f64(int32_t pos, uint64_t step, double& c, double& s) {
+    const uint64_t ph = (uint64_t)(int64_t)pos * step;
+    const double r = (double)(int64_t)ph * 0x1p-64;
+    sincospi(2.0 * r, &s, &c);
+}
+
+// cos/sin of N consecutive frequencies i0 .. i0+N-1 at position pos: from the table
+// when pos is inside it, else computed.
+template <int N, bool TABLE>
+__device__ __forceinline__ void rope_cs_n(const float* __restrict__ table, int rope_len, int half,
+                                          const uint64_t* fstep, int32_t pos, int i0, float* c, float* s) {
+    if (TABLE && (uint32_t)pos < (uint32_t)rope_len) {
+        const float4* t = reinterpret_cast<const float4*>(table + ((size_t)pos * half + i0) * 2);
+#pragma unroll
+        for (int k = 0; k < N / 2; ++k) {
+            const float4 v = t[k];
+            c[2 * k] = v.x; s[2 * k] = v.y; c[2 * k + 1] = v.z; s[2 * k + 1] = v.w;
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < N; ++k) rope_cs(pos, fstep[i0 + k], c[k], s[k]);
+    }
+}
+
+// ---------------------------------------------------------------------------------
+// kv_write: one thread per 16-byte chunk of a new row.
+// ---------------------------------------------------------------------------------
+__global__ void __launch_bounds__(256) kv_write_kernel(u32x4_t* __restrict__ k_pool, u32x4_t* __restrict__ v_pool,
+                                                       const u32x4_t* __restrict__ k_new,
+                                                       const u32x4_t* __restrict__ v_new,
+                                                       const int32_t* __restrict__ slots, int64_t n_chunks,
+                                                       int chunks_per_head, int hkv) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n_chunks) return;
+    const int64_t per_row = (int64_t)chunks_per_head * hkv;
+    const int64_t row = i / per_row;
+    const int rem = (int)(i - row * per_row);
+    const int h = rem / chunks_per_head, c = rem - h * chunks_per_head;
+    const int32_t slot = slots[row];
+    if (slot < 0) return;
+    const int64_t dst = (((int64_t)(slot >> 4) * hkv + h) * kBlock + (slot & 15)) * chunks_per_head + c;
+    k_pool[dst] = k_new[i];
+    v_pool[dst] = v_new[i];
+}
+
+// ---------------------------------------------------------------------------------
+// rope_table: entry [p][i] = (cos, sin)(p * omega_i), float64 math, float32 storage.
+// ---------------------------------------------------------------------------------
+__global__ void __launch_bounds__(256) rope_table_kernel(float2* __restrict__ table, int n_pos, int half, int d,
+                                                         double theta) {
+    const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= (int64_t)n_pos * half) return;
+    const int p = (int)(idx / half), i = (int)(idx - (int64_t)p * half);
+    double c, s;
+    rope_cs_f64(p, rope_phase_step(theta, i, d), c, s);
+    table[idx] = make_float2((float)c, (float)s);
+}
+
+// ---------------------------------------------------------------------------------
+// rope_rotate: x[row][h][:] <- R_{pos[row]} x[row][h][:], one thread per pair.
+// ---------------------------------------------------------------------------------
+template <typename T, int STYLE>
+__global__ void __launch_bounds__(256) rope_rotate_kernel(T* __restrict__ x, int64_t n_pairs, int heads, int d,
+                                                          double theta, const int32_t* __restrict__ positions,
+                                                          const float2* __restrict__ table, int rope_len) {
+    const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= n_pairs) return;
+    const int half = d / 2;
+    const int64_t rh = idx / half;                 // row * heads + h
+    const int i = (int)(idx - rh * half);
+    const int32_t pos = positions[rh / heads];
+    float c, s;
+    if (table != nullptr && (uint32_t)pos < (uint32_t)rope_len) {
+        const float2 v = table[(size_t)pos * half + i];
+        c = v.x; s = v.y;
+    } else {
+        rope_cs(pos, rope_phase_step(theta, i, d), c, s);
+    }
+    T* row = x + rh * d;
+    const int ia = STYLE == kNeox ? i : 2 * i, ib = STYLE == kNeox ? i + half : 2 * i + 1;
+    const float a = (float)row[ia], b = (float)row[ib];
+    row[ia] = (T)(a * c - b * s);
+    row[ib] = (T)(b * c + a * s);
+}
+
+// Locate the group of a block: groups are sorted by item_base.
+__device__ __forceinline__ int find_group(const Plan& plan, int bid) {
+    int gi = 0;
+    while (gi + 1 < plan.n_groups && plan.g[gi + 1].item_base <= bid) ++gi;
+    return gi;
+}
+
+__device__ __forceinline__ int find_merge_group(const Plan& plan, int bid) {
+    int gi = -1;
+    for (int i = 0; i < plan.n_groups; ++i)
+        if (plan.g[i].n_split > 1 && plan.g[i].merge_base <= bid) gi = i;
+    return gi;
+}
+
+// Bit-swap of the two 4-key groups in the middle of every 16 keys: the order in
+// which the PV contraction sees the keys a lane holds after QK^T (see below).
+__device__ __forceinline__ int vt_col(int k) {
+    const int g4 = (k >> 2) & 3;
+    return (k & ~15) | ((((g4 & 1) << 1) | (g4 >> 1)) << 2) | (k & 3);
+}
+
+// ---------------------------------------------------------------------------------
+// prefill_bf16
+//
+// Workgroup: 4 waves; wave w owns query rows [64w, 64w+64) of the tile as two
+// 32-column blocks.  Per 64-key tile:
+//   LDS ks[64][D]  rotated K (bf16), 16-byte chunks XOR-swizzled by row;
+//   LDS vt[D][64]  V transposed (bf16), key columns in vt_col order, swizzled.
+//   S^T (64 keys x 32 queries per block) = K Q^T with A = K from LDS and B = Q
+//   in registers: after the MFMA, lane l holds query column l%32 and keys
+//   8*(j/4) + 4*(l/32) + j%4 (j = 0..15) of each 32-key half, so row statistics
+//   need one exchange with lane l^32 only.  Those 16 values are exactly the B
+//   operand of O^T = V^T P^T for two 16-key steps once the contraction index is
+//   taken in vt_col order.
+// ---------------------------------------------------------------------------------
+template <int D, int STYLE, bool ROPE, bool TABLE>
+__global__ void __launch_bounds__(256, 1) prefill_bf16(const Plan plan, const Args a) {
+    constexpr int KD = D / 16;   // 16-wide contraction steps of QK^T
+    constexpr int DB = D / 32;   // 32-row blocks of O^T
+    constexpr int CH = D / 8;    // 16-byte chunks per K row
+    constexpr int HALF = D / 2;
+    constexpr int NB = 2;        // 32-query blocks per wave
+    constexpr int BN = kTileKeys;
+
+    __shared__ __attribute__((aligned(16))) uint16_t ks[BN * D];
+    __shared__ __attribute__((aligned(16))) uint16_t vt[D * BN];
+    __shared__ uint64_t fstep[HALF];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int l32 = lane & 31, hi = lane >> 5;
+
+    const int bid = blockIdx.x;
+    const Group g = plan.g[find_group(plan, bid)];
+    const int G = a.group;
+    const int n_clusters = a.hkv * g.n_split;
+    const int li = bid - g.item_base;
+    if (li >= n_clusters * g.n_rt) return;
+    int cluster, rt;
+    if ((n_clusters & 7) == 0) {
+        // blocks bid, bid+8, ... run on one XCD: give them the row tiles of one
+        // (KV head, split) so that they share K/V in that XCD's L2
+        const int x = li & 7, k = li >> 3;
+        cluster = x + 8 * (k / g.n_rt);
+        rt = k % g.n_rt;
+    } else {
+        cluster = li / g.n_rt;
+        rt = li % g.n_rt;
+    }
+    const int kvh = cluster / g.n_split, split = cluster - kvh * g.n_split;
+    const int rows_total = g.n_tok * G;
+    const int row_lo = rt * kTileRows;
+    const int row_hi = min(row_lo + kTileRows, rows_total);
+    const int t_last = g.tok0 + (row_hi - 1) / G;
+    const int kv_lo = g.win + split * g.split_keys;
+    const int kv_hi = min(kv_lo + g.split_keys, t_last + 1);
+    if (kv_lo >= kv_hi) return;
+
+    if (ROPE) {
+        for (int i = tid; i < HALF; i += 256) fstep[i] = rope_phase_step(a.theta, i, D);
+        __syncthreads();
+    }
+
+    // ---- queries: rotate at their positions, scale by softmax_scale*log2(e), bf16
+    bf16x8_t qb[NB][KD];
+    int row_tok[NB];
+    const int wave_row0 = row_lo + wave * 64;
+    const int wave_tmin = g.tok0 + min(wave_row0, row_hi - 1) / G;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+        const int row = wave_row0 + nb * 32 + l32;
+        const bool valid = row < row_hi;
+        const int toff = valid ? row / G : 0;
+        const int hl = valid ? row - toff * G : 0;
+        row_tok[nb] = valid ? g.tok0 + toff : t_last;
+        const uint16_t* qp = static_cast<const uint16_t*>(a.q) +
+                             ((size_t)(g.q_row0 + toff) * a.hq + (size_t)kvh * G + hl) * D;
+        u32x4_t raw[KD];
+#pragma unroll
+        for (int kd = 0; kd < KD; ++kd)
+            raw[kd] = valid ? *reinterpret_cast<const u32x4_t*>(qp + kd * 16 + 8 * hi) : u32x4_t{0, 0, 0, 0};
+        float xf[KD][8];
+#pragma unroll
+        for (int kd = 0; kd < KD; ++kd)
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+                xf[kd][2 * m] = bf_lo(raw[kd][m]);
+                xf[kd][2 * m + 1] = bf_hi(raw[kd][m]);
+            }
+        if (ROPE) {
+            const int32_t pos = valid ? a.positions[g.pos_off + g.tok0 + toff] : 0;
+            if (STYLE == kNeox) {
+#pragma unroll
+                for (int kd = 0; kd < KD / 2; ++kd) {
+                    float c[8], s[8];
+                    rope_cs_n<8, TABLE>(a.rope_table, a.rope_len, HALF, fstep, pos, kd * 16 + 8 * hi, c, s);
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const float x = xf[kd][e], y = xf[kd + KD / 2][e];
+                        xf[kd][e] = x * c[e] - y * s[e];
+                        xf[kd + KD / 2][e] = y * c[e] + x * s[e];
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int kd = 0; kd < KD; ++kd) {
+                    float c[4], s[4];
+                    rope_cs_n<4, TABLE>(a.rope_table, a.rope_len, HALF, fstep, pos, kd * 8 + 4 * hi, c, s);
+#pragma unroll
+                    for (int m = 0; m < 4; ++m) {
+                        const float x = xf[kd][2 * m], y = xf[kd][2 * m + 1];
+                        xf[kd][2 * m] = x * c[m] - y * s[m];
+                        xf[kd][2 * m + 1] = y * c[m] + x * s[m];
+                    }
+                }
+            }
+        }
+#pragma unroll
+        for (int kd = 0; kd < KD; ++kd) {
+            u32x4_t w;
+#pragma unroll
+            for (int m = 0; m < 4; ++m)
+                w[m] = pack_bf16(xf[kd][2 * m] * a.scale_log2, xf[kd][2 * m + 1] * a.scale_log2);
+            qb[nb][kd] = __builtin_bit_cast(bf16x8_t, w);
+        }
+    }
+
+    f32x16_t acc[NB][DB];
+    float m_run[NB], l_run[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+        m_run[nb] = kNegBig;
+        l_run[nb] = 0.f;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) acc[nb][db] = f32x16_t{};
+    }
+
+    const int32_t* btab = a.block_tables + (size_t)g.req * a.max_blocks;
+    const uint16_t* kpool = static_cast<const uint16_t*>(a.k_pool);
+    const uint16_t* vpool = static_cast<const uint16_t*>(a.v_pool);
+
+    for (int kt = kv_lo & ~(kBlock - 1); kt < kv_hi; kt += BN) {
+        __syncthreads();  // the previous tile is consumed
+        // ---- K tile: gather, rotate at the keys' positions, bf16 into LDS
+        constexpr int KU = BN * (D / 16);
+#pragma unroll
+        for (int u0 = 0; u0 < KU / 256; ++u0) {
+            const int u = tid + u0 * 256;
+            const int kk = u / (D / 16), c = u - kk * (D / 16);
+            const int j = kt + kk;
+            const bool ok = j >= kv_lo && j < kv_hi;
+            u32x4_t xa = {0, 0, 0, 0}, xb = {0, 0, 0, 0};
+            if (ok) {
+                const int phys = btab[j >> 4];
+                const uint16_t* src = kpool + (((size_t)phys * a.hkv + kvh) * kBlock + (j & 15)) * D;
+                if (STYLE == kNeox) {
+                    xa = *reinterpret_cast<const u32x4_t*>(src + c * 8);
+                    xb = *reinterpret_cast<const u32x4_t*>(src + HALF + c * 8);
+                } else {
+                    xa = *reinterpret_cast<const u32x4_t*>(src + c * 16);
+                    xb = *reinterpret_cast<const u32x4_t*>(src + c * 16 + 8);
+                }
+                if (ROPE) {
+                    const int32_t pos = a.positions[g.pos_off + j];
+                    float cs[8], sn[8];
+                    rope_cs_n<8, TABLE>(a.rope_table, a.rope_len, HALF, fstep, pos, c * 8, cs, sn);
+                    if (STYLE == kNeox) {
+#pragma unroll
+                        for (int m = 0; m < 4; ++m) {
+                            const float x0 = bf_lo(xa[m]), x1 = bf_hi(xa[m]);
+                            const float y0 = bf_lo(xb[m]), y1 = bf_hi(xb[m]);
+                            const float c0 = cs[2 * m], c1 = cs[2 * m + 1], s0 = sn[2 * m], s1 = sn[2 * m + 1];
+                            xa[m] = pack_bf16(x0 * c0 - y0 * s0, x1 * c1 - y1 * s1);
+                            xb[m] = pack_bf16(y0 * c0 + x0 * s0, y1 * c1 + x1 * s1);
+                        }
+                    } else {
+#pragma unroll
+                        for (int m = 0; m < 4; ++m) {
+                            const float x0 = bf_lo(xa[m]), y0 = bf_hi(xa[m]);
+                            xa[m] = pack_bf16(x0 * cs[m] - y0 * sn[m], y0 * cs[m] + x0 * sn[m]);
+                            const float x1 = bf_lo(xb[m]), y1 = bf_hi(xb[m]);
+                            xb[m] = pack_bf16(x1 * cs[4 + m] - y1 * sn[4 + m], y1 * cs[4 + m] + x1 * sn[4 + m]);
+                        }
+                    }
+                }
+            }
+            const int ca = STYLE == kNeox ? c : 2 * c;
+            const int cb = STYLE == kNeox ? c + CH / 2 : 2 * c + 1;
+            const int sw = kk & (CH - 1);
+            *reinterpret_cast<u32x4_t*>(ks + kk * D + ((ca ^ sw) << 3)) = xa;
+            *reinterpret_cast<u32x4_t*>(ks + kk * D + ((cb ^ sw) << 3)) = xb;
+        }
+        // ---- V tile: gather 4 keys x 8 dims per thread, transpose into vt
+        constexpr int VU = (BN / 4) * CH;
+        if (tid < VU) {
+            const int kg = tid / CH, dc = tid - kg * CH;
+            u32x4_t r[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int j = kt + kg * 4 + e;
+                r[e] = u32x4_t{0, 0, 0, 0};
+                if (j >= kv_lo && j < kv_hi) {
+                    const int phys = btab[j >> 4];
+                    r[e] = *reinterpret_cast<const u32x4_t*>(
+                        vpool + (((size_t)phys * a.hkv + kvh) * kBlock + (j & 15)) * D + dc * 8);
+                }
+            }
+            const int col = vt_col(kg * 4);
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+                const u32x2_t lo = {(r[0][m] & 0xffffu) | (r[1][m] << 16), (r[2][m] & 0xffffu) | (r[3][m] << 16)};
+                const u32x2_t hv = {(r[0][m] >> 16) | (r[1][m] & 0xffff0000u),
+                                    (r[2][m] >> 16) | (r[3][m] & 0xffff0000u)};
+                const int d0 = dc * 8 + 2 * m, d1 = d0 + 1;
+                *reinterpret_cast<u32x2_t*>(vt + d0 * BN + ((((col >> 3) ^ (d0 & 7)) << 3) | (col & 7))) = lo;
+                *reinterpret_cast<u32x2_t*>(vt + d1 * BN + ((((col >> 3) ^ (d1 & 7)) << 3) | (col & 7))) = hv;
+            }
+        }
+        __syncthreads();
+
+        // ---- S^T = K Q^T
+        f32x16_t s[NB][2];
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) s[nb][0] = s[nb][1] = f32x16_t{};
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb) {
+            const int kr = mb * 32 + l32;
+#pragma unroll
+            for (int kd = 0; kd < KD; ++kd) {
+                const bf16x8_t af = *reinterpret_cast<const bf16x8_t*>(
+                    ks + kr * D + (((kd * 2 + hi) ^ (kr & (CH - 1))) << 3));
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb)
+                    s[nb][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, qb[nb][kd], s[nb][mb], 0, 0, 0);
+            }
+        }
+
+        // ---- window mask (only on tiles that cross a boundary of the visible set)
+        const bool need_mask = kt < kv_lo || kt + BN > kv_hi || kt + BN - 1 > wave_tmin;
+        if (need_mask) {
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+                    for (int j = 0; j < 16; ++j) {
+                        const int key = kt + mb * 32 + 8 * (j >> 2) + 4 * hi + (j & 3);
+                        if (key < kv_lo || key >= kv_hi || key > row_tok[nb]) s[nb][mb][j] = -INFINITY;
+                    }
+        }
+
+        // ---- online softmax (log2 domain)
+        bf16x8_t pb[NB][2][2];
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+            float mx = kNegBig;
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+                for (int j = 0; j < 16; ++j) mx = fmaxf(mx, s[nb][mb][j]);
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            const float m_new = fmaxf(m_run[nb], mx);
+            const float alpha = __builtin_amdgcn_exp2f(m_run[nb] - m_new);
+            float ls = 0.f;
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb) {
+#pragma unroll
+                for (int j = 0; j < 16; ++j) {
+                    const float p = __builtin_amdgcn_exp2f(s[nb][mb][j] - m_new);
+                    s[nb][mb][j] = p;
+                    ls += p;
+                }
+#pragma unroll
+                for (int ks2 = 0; ks2 < 2; ++ks2) {
+                    u32x4_t w;
+#pragma unroll
+                    for (int m = 0; m < 4; ++m)
+                        w[m] = pack_bf16(s[nb][mb][8 * ks2 + 2 * m], s[nb][mb][8 * ks2 + 2 * m + 1]);
+                    pb[nb][mb][ks2] = __builtin_bit_cast(bf16x8_t, w);
+                }
+            }
+            l_run[nb] = l_run[nb] * alpha + ls;
+            m_run[nb] = m_new;
+#pragma unroll
+            for (int db = 0; db < DB; ++db) acc[nb][db] *= alpha;
+        }
+
+        // ---- O^T += V^T P^T
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+            const int dr = db * 32 + l32;
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+                for (int ks2 = 0; ks2 < 2; ++ks2) {
+                    const int chunk = mb * 4 + ks2 * 2 + hi;
+                    const bf16x8_t af = *reinterpret_cast<const bf16x8_t*>(vt + dr * BN + ((chunk ^ (dr & 7)) << 3));
+#pragma unroll
+                    for (int nb = 0; nb < NB; ++nb)
+                        acc[nb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, pb[nb][mb][ks2], acc[nb][db], 0, 0, 0);
+                }
+        }
+    }
+
+    // ---- epilogue: normalise and store, or store the split's partial state
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+        const float lt = l_run[nb] + __shfl_xor(l_run[nb], 32);
+        const int row = wave_row0 + nb * 32 + l32;
+        if (row >= row_hi) continue;
+        if (g.n_split == 1) {
+            const float inv = 1.f / lt;
+            const int toff = row / G, hl = row - toff * G;
+            uint16_t* op = static_cast<uint16_t*>(a.o) + ((size_t)(g.q_row0 + toff) * a.hq + (size_t)kvh * G + hl) * D;
+#pragma unroll
+            for (int db = 0; db < DB; ++db)
+#pragma unroll
+                for (int q4 = 0; q4 < 4; ++q4) {
+                    const int d = db * 32 + 8 * q4 + 4 * hi;
+                    const u32x2_t w = {pack_bf16(acc[nb][db][4 * q4] * inv, acc[nb][db][4 * q4 + 1] * inv),
+                                       pack_bf16(acc[nb][db][4 * q4 + 2] * inv, acc[nb][db][4 * q4 + 3] * inv)};
+                    *reinterpret_cast<u32x2_t*>(op + d) = w;
+                }
+        } else {
+            const size_t slot = (size_t)g.part_base + (size_t)cluster * g.n_rt + rt;
+            float* po = a.part_o + (slot * kTileRows + (row - row_lo)) * D;
+#pragma unroll
+            for (int db = 0; db < DB; ++db)
+#pragma unroll
+                for (int q4 = 0; q4 < 4; ++q4) {
+                    const int d = db * 32 + 8 * q4 + 4 * hi;
+                    *reinterpret_cast<float4*>(po + d) =
+                        make_float4(acc[nb][db][4 * q4], acc[nb][db][4 * q4 + 1], acc[nb][db][4 * q4 + 2],
+                                    acc[nb][db][4 * q4 + 3]);
+                }
+            if (hi == 0)
+                *reinterpret_cast<float2*>(a.part_ml + (slot * kTileRows + (row - row_lo)) * 2) =
+                    make_float2(m_run[nb], lt);
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------------
+// merge: O = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s over the non-empty splits
+// of one (row tile, KV head); one block per pair.
+// ---------------------------------------------------------------------------------
+template <int D, typename TO>
+__global__ void __launch_bounds__(256) merge_kernel(const Plan plan, const Args a) {
+    const int gi = find_merge_group(plan, blockIdx.x);
+    if (gi < 0) return;
+    const Group g = plan.g[gi];
+    const int li = blockIdx.x - g.merge_base;
+    if (li >= a.hkv * g.n_rt) return;
+    const int kvh = li / g.n_rt, rt = li - kvh * g.n_rt;
+    const int G = a.group;
+    const int row_lo = rt * kTileRows;
+    const int row_hi = min(row_lo + kTileRows, g.n_tok * G);
+    const int t_last = g.tok0 + (row_hi - 1) / G;
+    int n_live = 0;
+    for (int s = 0; s < g.n_split; ++s)
+        if (g.win + s * g.split_keys < t_last + 1) n_live = s + 1;
+    constexpr int Q4 = D / 4;
+    for (int u = threadIdx.x; u < (row_hi - row_lo) * Q4; u += blockDim.x) {
+        const int r = u / Q4, q4 = u - r * Q4;
+        float mmax = kNegBig;
+        for (int s = 0; s < n_live; ++s) {
+            const size_t slot = (size_t)g.part_base + ((size_t)kvh * g.n_split + s) * g.n_rt + rt;
+            const float2 ml = *reinterpret_cast<const float2*>(a.part_ml + (slot * kTileRows + r) * 2);
+            if (ml.y > 0.f) mmax = fmaxf(mmax, ml.x);
+        }
+        float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
+        float den = 0.f;
+        for (int s = 0; s < n_live; ++s) {
+            const size_t slot = (size_t)g.part_base + ((size_t)kvh * g.n_split + s) * g.n_rt + rt;
+            const float2 ml = *reinterpret_cast<const float2*>(a.part_ml + (slot * kTileRows + r) * 2);
+            if (!(ml.y > 0.f)) continue;
+            const float w = __builtin_amdgcn_exp2f(ml.x - mmax);
+            const float4 v = *reinterpret_cast<const float4*>(a.part_o + (slot * kTileRows + r) * D + q4 * 4);
+            num.x += w * v.x; num.y += w * v.y; num.z += w * v.z; num.w += w * v.w;
+            den += w * ml.y;
+        }
+        const float inv = 1.f / den;
+        const int row = row_lo + r;
+        const int toff = row / G, hl = row - toff * G;
+        TO* op = static_cast<TO*>(a.o) + ((size_t)(g.q_row0 + toff) * a.hq + (size_t)kvh * G + hl) * D + q4 * 4;
+        op[0] = (TO)(num.x * inv);
+        op[1] = (TO)(num.y * inv);
+        op[2] = (TO)(num.z * inv);
+        op[3] = (TO)(num.w * inv);
+    }
+}
+
+// ---------------------------------------------------------------------------------
+// attn_f32: one wave per (query token, query head); lane holds D/64 elements.
+// ---------------------------------------------------------------------------------
+template <int D, int STYLE, bool ROPE, bool TABLE>
+__global__ void __launch_bounds__(64) attn_f32(const Plan plan, const Args a) {
+    constexpr int E = D / 64;
+    constexpr int HALF = D / 2;
+    const int lane = threadIdx.x;
+    const int bid = blockIdx.x;
+    const Group g = plan.g[find_group(plan, bid)];
+    const int li = bid - g.item_base;
+    if (li >= g.n_tok * a.hq) return;
+    const int toff = li / a.hq, h = li - toff * a.hq;
+    const int kvh = h / a.group;
+    const int t = g.tok0 + toff;
+
+    // element e of this lane is dimension d = lane + 64 e; its pair partner and
+    // frequency follow the pairing style
+    auto partner_val = [&](const float* v, int e) -> float {
+        if (STYLE == kNeox) {
+            if (E == 2) return v[1 - e];
+            return __shfl_xor(v[e], 32);
+        }
+        return __shfl_xor(v[e], 1);
+    };
+    auto rotate = [&](float* v, int32_t pos) {
+        float pv[E];
+#pragma unroll
+        for (int e = 0; e < E; ++e) pv[e] = partner_val(v, e);
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            const int d = lane + 64 * e;
+            const int i = STYLE == kNeox ? (d % HALF) : d / 2;
+            const bool first = STYLE == kNeox ? d < HALF : (d & 1) == 0;
+            float c, s;
+            if (TABLE && (uint32_t)pos < (uint32_t)a.rope_len) {
+                const float2 cs = reinterpret_cast<const float2*>(a.rope_table)[(size_t)pos * HALF + i];
+                c = cs.x; s = cs.y;
+            } else {
+                rope_cs(pos, rope_phase_step(a.theta, i, D), c, s);
+            }
+            v[e] = first ? v[e] * c - pv[e] * s : v[e] * c + pv[e] * s;
+        }
+    };
+
+    const float* qp = static_cast<const float*>(a.q) + ((size_t)(g.q_row0 + toff) * a.hq + h) * D;
+    float q[E], o[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        q[e] = qp[lane + 64 * e];
+        o[e] = 0.f;
+    }
+    if (ROPE) rotate(q, a.positions[g.pos_off + t]);
+#pragma unroll
+    for (int e = 0; e < E; ++e) q[e] *= a.scale_log2;
+
+    const int32_t* btab = a.block_tables + (size_t)g.req * a.max_blocks;
+    const float* kpool = static_cast<const float*>(a.k_pool);
+    const float* vpool = static_cast<const float*>(a.v_pool);
+    float m = kNegBig, l = 0.f;
+    for (int j = g.win; j <= t; ++j) {
+        const size_t base = (((size_t)btab[j >> 4] * a.hkv + kvh) * kBlock + (j & 15)) * D;
+        float k[E], v[E];
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            k[e] = kpool[base + lane + 64 * e];
+            v[e] = vpool[base + lane + 64 * e];
+        }
+        if (ROPE) rotate(k, a.positions[g.pos_off + j]);
+        float sc = 0.f;
+#pragma unroll
+        for (int e = 0; e < E; ++e) sc += q[e] * k[e];
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) sc += __shfl_xor(sc, off);
+        const float m_new = fmaxf(m, sc);
+        const float alpha = exp2f(m - m_new), p = exp2f(sc - m_new);
+        l = l * alpha + p;
+#pragma unroll
+        for (int e = 0; e < E; ++e) o[e] = o[e] * alpha + p * v[e];
+        m = m_new;
+    }
+    float* op = static_cast<float*>(a.o) + ((size_t)(g.q_row0 + toff) * a.hq + h) * D;
+#pragma unroll
+    for (int e = 0; e < E; ++e) op[lane + 64 * e] = o[e] / l;
+}
+
+template <int D, int STYLE, bool ROPE, bool TABLE>
+hipError_t launch_attn_t(int dtype, const Plan& plan, const Args& a, hipStream_t st) {
+    if (dtype == 1) {
+        hipLaunchKernelGGL((attn_f32<D, STYLE, ROPE, TABLE>), dim3(plan.n_items), dim3(64), 0, st, plan, a);
+        return hipGetLastError();
+    }
+    hipLaunchKernelGGL((prefill_bf16<D, STYLE, ROPE, TABLE>), dim3(plan.n_items), dim3(256), 0, st, plan, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (plan.n_merge > 0) {
+        hipLaunchKernelGGL((merge_kernel<D, __bf16>), dim3(plan.n_merge), dim3(256), 0, st, plan, a);
+        e = hipGetLastError();
+    }
+    return e;
+}
+
+template <int D, int STYLE>
+hipError_t launch_attn_d(int dtype, bool rope, const Plan& plan, const Args& a, hipStream_t st) {
+    const bool table = a.rope_table != nullptr && a.rope_len > 0;
+    if (!rope) return launch_attn_t<D, STYLE, false, false>(dtype, plan, a, st);
+    return table ? launch_attn_t<D, STYLE, true, true>(dtype, plan, a, st)
+                 : launch_attn_t<D, STYLE, true, false>(dtype, plan, a, st);
+}
+
+}  // namespace
+
+int launch_kv_write(int dtype, int hkv, int d, void* k_pool, void* v_pool, const void* k_new, const void* v_new,
+                    const int32_t* slots, int n, void* stream) {
+    const int esize = dtype == 1 ? 4 : 2;
+    const int chunks_per_head = d * esize / 16;
+    const int64_t n_chunks = (int64_t)n * hkv * chunks_per_head;
+    if (n_chunks == 0) return hipSuccess;
+    const int64_t blocks = (n_chunks + 255) / 256;
+    hipLaunchKernelGGL(kv_write_kernel, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream,
+                       static_cast<u32x4_t*>(k_pool), static_cast<u32x4_t*>(v_pool),
+                       static_cast<const u32x4_t*>(k_new), static_cast<const u32x4_t*>(v_new), slots, n_chunks,
+                       chunks_per_head, hkv);
+    return hipGetLastError();
+}
+
+int launch_rope_table(int d, double theta, int n_pos, float* table, void* stream) {
+    const int64_t n = (int64_t)n_pos * (d / 2);
+    if (n == 0) return hipSuccess;
+    hipLaunchKernelGGL(rope_table_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, (hipStream_t)stream,
+                       reinterpret_cast<float2*>(table), n_pos, d / 2, d, theta);
+    return hipGetLastError();
+}
+
+int launch_rope_rotate(int dtype, int style, int d, double theta, const float* table, int rope_len, void* x, int n,
+                       int heads, const int32_t* positions, void* stream) {
+    const int64_t n_pairs = (int64_t)n * heads * (d / 2);
+    if (n_pairs == 0) return hipSuccess;
+    const dim3 grid((unsigned)((n_pairs + 255) / 256));
+    const float2* t = reinterpret_cast<const float2*>(table);
+    hipStream_t st = (hipStream_t)stream;
+    if (dtype == 1) {
+        if (style == kNeox)
+            hipLaunchKernelGGL((rope_rotate_kernel<float, 0>), grid, dim3(256), 0, st, static_cast<float*>(x),
+                               n_pairs, heads, d, theta, positions, t, rope_len);
+        else
+            hipLaunchKernelGGL((rope_rotate_kernel<float, 1>), grid, dim3(256), 0, st, static_cast<float*>(x),
+                               n_pairs, heads, d, theta, positions, t, rope_len);
+    } else {
+        if (style == kNeox)
+            hipLaunchKernelGGL((rope_rotate_kernel<__bf16, 0>), grid, dim3(256), 0, st, static_cast<__bf16*>(x),
+                               n_pairs, heads, d, theta, positions, t, rope_len);
+        else
+            hipLaunchKernelGGL((rope_rotate_kernel<__bf16, 1>), grid, dim3(256), 0, st, static_cast<__bf16*>(x),
+                               n_pairs, heads, d, theta, positions, t, rope_len);
+    }
+    return hipGetLastError();
+}
+
+int launch_attention(int dtype, int style, int d, bool rope, const Plan& plan, const Args& args, void* stream) {
+    if (plan.n_items == 0) return hipSuccess;
+    hipStream_t st = (hipStream_t)stream;
+    if (d == 64)
+        return style == kNeox ? launch_attn_d<64, 0>(dtype, rope, plan, args, st)
+                              : launch_attn_d<64, 1>(dtype, rope, plan, args, st);
+    return style == kNeox ? launch_attn_d<128, 0>(dtype, rope, plan, args, st)
+                          : launch_attn_d<128, 1>(dtype, rope, plan, args, st);
+}
+
+}  // namespace pic

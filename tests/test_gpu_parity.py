@@ -1,0 +1,208 @@
+"""GPU parity: libpic_attn against the fp64 oracle on the same seeded inputs."""
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from oracle import pic_oracle as O
+from oracle import workload_oracle as WO
+from tests.gpu_util import assert_close, gpu_run, say, to_np
+
+pytestmark = pytest.mark.gpu
+
+S, Pd, Q, Sp = W.SSEP, W.PDEP, W.QUERY, W.Span
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2606_13126_amd  # noqa: F401  (fails loudly if the library is missing)
+
+
+def check(wl, style=0, table=True, rows=None, what=None):
+    what = what or wl.name
+    say(f"[gpu] {what}: shape q={tuple(wl.q.shape)} dtype={wl.dtype} style={style} table={table}")
+    db = gpu_run(wl, rope_style=style, table=table)
+    got = to_np(db.o)
+    ref = WO.run(wl, rows=rows, style="neox" if style == 0 else "gptj")
+    if rows is not None:
+        got = got[rows]
+    return assert_close(got, ref, wl.dtype, what)
+
+
+@pytest.mark.parametrize("tail_only", [False, True])
+@pytest.mark.parametrize("table", [True, False])
+def test_config0_fp32(tail_only, table):
+    check(W.config0(tail_only=tail_only), table=table)
+
+
+def test_kv_write_bit_exact():
+    for wl in (W.config0(), W.config1()):
+        db = gpu_run(wl)
+        k_ref, v_ref = wl.k_pool.clone(), wl.v_pool.clone()
+        iv = torch.int32 if wl.dtype == torch.float32 else torch.int16
+        kr, vr = k_ref.view(iv).numpy(), v_ref.view(iv).numpy()
+        O.kv_write(kr, vr, wl.k_new.view(iv).numpy(), wl.v_new.view(iv).numpy(), wl.slot_mapping)
+        assert np.array_equal(db.k_pool.cpu().view(iv).numpy(), kr)
+        assert np.array_equal(db.v_pool.cpu().view(iv).numpy(), vr)
+
+
+@pytest.mark.parametrize("table", [True, False])
+def test_config1_bf16(table):
+    check(W.config1(), table=table)
+
+
+def test_config2_bf16():
+    check(W.config2())
+
+
+def test_config3_decode_bf16():
+    check(W.config3())
+
+
+def test_config4_sampled_rows():
+    wl = W.config4()
+    rng = np.random.default_rng(4)
+    n = wl.q.shape[0]
+    rows = np.unique(np.concatenate([rng.choice(n, 48, replace=False), [0, n - 1, n - 512, n - 513, 511, 512]]))
+    check(wl, rows=rows)
+
+
+@pytest.mark.parametrize("style", [0, 1])
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_unaligned_spans_gqa(style, dtype):
+    wl = W.small_case("unaligned", [[Sp(21, S | Q, fresh=True), Sp(37, Q, fresh=True), Sp(300, S | Q, fresh=True),
+                                     Sp(11, Pd | Q, fresh=True)]], Hq=8, Hkv=2, D=128, theta=1e4, dtype=dtype,
+                      seed=5, value_scale=0.5)
+    check(wl, style=style)
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_mha_d64_multi_request(dtype):
+    reqs = [[Sp(64, S, key="a"), Sp(48, S, key="b"), Sp(70, Pd | Q, fresh=True)],
+            [Sp(48, S, key="b"), Sp(64, S, key="a"), Sp(5, Pd | Q, fresh=True)],
+            [Sp(32, S, key="c")] + [Sp(16, S | Q, fresh=True)],
+            [Sp(9, S, key=None), Sp(40, Q, fresh=True)]]
+    wl = W.small_case("mha", reqs, Hq=4, Hkv=4, D=64, theta=1e4, dtype=dtype, seed=6, value_scale=0.5)
+    check(wl)
+
+
+def test_zero_query_request_and_empty_batch():
+    reqs = [[Sp(32, S, key="a")], [Sp(32, S, key="a"), Sp(17, Pd | Q, fresh=True)], [Sp(16, S)]]
+    wl = W.small_case("zq", reqs, Hq=8, Hkv=2, D=128, dtype=torch.bfloat16, seed=7, value_scale=0.5)
+    check(wl)
+
+
+def test_first_token_of_ssep_span_is_its_value():
+    wl = W.small_case("first", [[Sp(32, S | Q, fresh=True), Sp(48, S | Q, fresh=True)]], Hq=4, Hkv=1, D=128,
+                      dtype=torch.bfloat16, seed=8, value_scale=0.5)
+    db = gpu_run(wl)
+    o = db.o.cpu()
+    for t in (0, 32):
+        assert torch.equal(o[t], wl.v_new[t, 0].expand(4, 128)), t
+
+
+def test_excluded_blocks_are_never_read():
+    # span 1 is detached (SSEP) from span 0, whose blocks hold NaN: output must be finite
+    wl = W.small_case("poison", [[Sp(64, S, key="a"), Sp(96, S | Q, fresh=True), Sp(32, S | Q, fresh=True)]],
+                      Hq=8, Hkv=2, D=128, dtype=torch.bfloat16, seed=9, value_scale=0.5)
+    for b in wl.block_tables[0][:4]:
+        wl.k_pool[b] = float("nan")
+        wl.v_pool[b] = float("nan")
+    check(wl, what="poisoned excluded span")
+
+
+def test_duplicate_block_in_one_request():
+    wl = W.small_case("dup", [[Sp(64, S, key="a"), Sp(64, S, key="a"), Sp(40, Pd | Q, fresh=True)]], Hq=8, Hkv=2,
+                      D=128, dtype=torch.bfloat16, seed=10, value_scale=0.5)
+    assert wl.block_tables[0][0] == wl.block_tables[0][4]
+    check(wl)
+
+
+def test_shift_invariance_bf16():
+    wl = W.small_case("shift", [[Sp(128, S, key="a"), Sp(200, S | Q, fresh=True), Sp(64, Pd | Q, fresh=True)]],
+                      Hq=8, Hkv=2, D=128, theta=5e5, dtype=torch.bfloat16, seed=11, value_scale=0.5)
+    base = to_np(gpu_run(wl).o)
+    for shift in (1000, 65536, -37):
+        wl.positions = (wl.positions.astype(np.int64) + shift).astype(np.int32)
+        got = to_np(gpu_run(wl).o)    # table for non-negative positions, computed otherwise
+        assert_close(got, base, wl.dtype, f"shift {shift} vs unshifted")
+        wl.positions = (wl.positions.astype(np.int64) - shift).astype(np.int32)
+    ref = WO.run(wl)
+    assert_close(base, ref, wl.dtype, "unshifted vs oracle")
+
+
+def test_concurrent_reuse_equals_alone():
+    wl = W.config2(num_reqs=4, pool_spans=6, per_req=3, span_len=256, tail=64)
+    full = to_np(gpu_run(wl).o)
+    row = 0
+    for r in range(wl.num_reqs):
+        sl = slice(wl.cu_spans[r], wl.cu_spans[r + 1])
+        nq = 64
+        one = W.Workload(**{**wl.__dict__})
+        one.seq_lens = wl.seq_lens[r:r + 1]
+        one.cu_spans = np.array([0, sl.stop - sl.start], np.int32)
+        one.span_start, one.span_flags = wl.span_start[sl], wl.span_flags[sl]
+        one.block_tables = wl.block_tables[r:r + 1]
+        off = wl.seq_offsets
+        one.positions = wl.positions[off[r]:off[r + 1]]
+        one.q = wl.q[row:row + nq]
+        one.k_new, one.v_new = wl.k_new[row:row + nq], wl.v_new[row:row + nq]
+        one.slot_mapping = wl.slot_mapping[row:row + nq]
+        alone = to_np(gpu_run(one).o)
+        assert_close(alone, full[row:row + nq], wl.dtype, f"request {r} alone vs batched")
+        row += nq
+
+
+def test_decode_equals_prefill_of_last_token():
+    dec = W.config3(num_reqs=3, num_spans=4, span_len=128)
+    od = to_np(gpu_run(dec).o)
+    pre = W.Workload(**{**dec.__dict__})
+    pre.is_decode = False
+    pre.span_flags = dec.span_flags.copy()
+    last = dec.cu_spans[1:] - 1
+    pre.span_flags[last] |= W.QUERY
+    op = to_np(gpu_run(pre).o)
+    assert_close(od, op, dec.dtype, "decode vs prefill of the last token")
+    assert_close(od, WO.run(dec), dec.dtype, "decode vs oracle")
+
+
+def test_fused_rope_equals_prerotated_baseline():
+    # Sec. 3.2.1: rotating inside attention equals attention over pre-rotated keys
+    import paper_2606_13126_amd as P
+    from paper_2606_13126_amd.runner import DeviceBatch
+    wl = W.small_case("pre", [[Sp(128, S, key="a"), Sp(256, S | Q, fresh=True), Sp(100, Pd | Q, fresh=True)]],
+                      Hq=8, Hkv=2, D=128, theta=5e5, dtype=torch.bfloat16, seed=12, value_scale=0.5)
+    fused = gpu_run(wl)
+    ctl = DeviceBatch(wl, k_prerotated=True, table_positions=int(wl.positions.max()) + 1)
+    ctl.write()
+    # rotate every stored key at its position (all slots of the request) and the queries
+    L = int(wl.seq_lens[0])
+    n = torch.arange(L)
+    slots = (torch.from_numpy(wl.block_tables[0].astype(np.int64))[n // 16] * 16 + n % 16)
+    pos = torch.from_numpy(wl.positions[:L]).cuda()
+    kp = ctl.k_pool.permute(0, 2, 1, 3).reshape(-1, wl.num_kv_heads, wl.head_dim)
+    rows = kp[slots.cuda()].contiguous()
+    P.pic_rope_rotate(ctl.cfg, rows, pos, table=ctl.table)
+    kp[slots.cuda()] = rows
+    ctl.k_pool = kp.reshape(-1, 16, wl.num_kv_heads, wl.head_dim).permute(0, 2, 1, 3).contiguous()
+    qpos = torch.from_numpy(wl.q_tokens[:, 1].astype(np.int32)).cuda()
+    qpos = pos[qpos.long()].contiguous()
+    P.pic_rope_rotate(ctl.cfg, ctl.q, qpos, table=ctl.table)
+    ctl.attend()
+    torch.cuda.synchronize()
+    assert_close(to_np(ctl.o), to_np(fused.o), wl.dtype, "pre-rotated baseline vs fused")
+    assert_close(to_np(fused.o), WO.run(wl), wl.dtype, "fused vs oracle")
+
+
+def test_rope_table_accuracy():
+    import paper_2606_13126_amd as P
+    cfg = P.make_config(8, 8, 128, rope_theta=5e5)
+    n = 40000
+    tab = torch.empty((n, 64, 2), dtype=torch.float32, device="cuda")
+    P.pic_rope_table_build(cfg, tab)
+    got = tab.cpu().double().numpy()
+    p = np.arange(n, dtype=np.float64)[:, None] * O.rope_inv_freq(128, 5e5)[None, :]
+    assert np.max(np.abs(got[..., 0] - np.cos(p))) <= 1e-7
+    assert np.max(np.abs(got[..., 1] - np.sin(p))) <= 1e-7
