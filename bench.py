@@ -1,0 +1,217 @@
+"""Benchmark of position-free paged attention on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--no-extra]
+
+A step is one pass of the hot path over one synthetic batch of the
+Llama-3-8B-shaped RAG prefill (10 cached 512-token SSEP spans, a fresh 256-token
+PDEP query tail, 32/8 heads, head_dim 128, theta 5e5, bf16): pic_kv_write of the
+tail's K/V rows followed by pic_attn_prefill.  Inputs are resident in HBM before
+the timed region.  ``value`` is the algorithmic prefill work (4*D*Hq per visible
+query/key pair) per step time, in TFLOP/s.  Extra fields time every workload,
+the fused-RoPE overhead against the same kernel on pre-rotated K, the decode
+bandwidth, and the fp64 CPU oracle on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import workloads as W  # noqa: E402
+
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+METRIC = "prefill attn TFLOP/s (% bf16 MFMA peak) + decode GB/s; fused-RoPE overhead %"
+
+
+def flops_of(wl) -> float:
+    """4 * D * Hq * (visible query/key pairs): counted from the span windows."""
+    total = 0
+    for r in range(wl.num_reqs):
+        L = int(wl.seq_lens[r])
+        sl = slice(wl.cu_spans[r], wl.cu_spans[r + 1])
+        st, fl = wl.span_start[sl], wl.span_flags[sl]
+        prev = 0
+        for k in range(len(st)):
+            b, e = int(st[k]), (int(st[k + 1]) if k + 1 < len(st) else L)
+            f = int(fl[k])
+            w = b if f & W.SSEP else (0 if f & W.PDEP else prev)
+            prev = w
+            if wl.is_decode:
+                if e == L:
+                    total += L - w
+            elif f & W.QUERY:
+                total += sum(t - w + 1 for t in range(b, e))
+    return 4.0 * wl.head_dim * wl.num_q_heads * total
+
+
+def decode_bytes(wl) -> float:
+    """K and V rows read once per request and KV head, plus q/o, positions, tables."""
+    esize = 2 if wl.dtype == torch.bfloat16 else 4
+    kv = float(np.sum(wl.seq_lens)) * wl.num_kv_heads * wl.head_dim * 2 * esize
+    qo = 2.0 * wl.q.numel() * esize
+    meta = 4.0 * float(np.sum(wl.seq_lens)) + 4.0 * wl.block_tables.size
+    return kv + qo + meta
+
+
+def timed(fn, steps, warmup, stream):
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for a, b in ev:
+        a.record(stream)
+        fn()
+        b.record(stream)
+    torch.cuda.synchronize()
+    ms = np.array([a.elapsed_time(b) for a, b in ev])
+    return ms
+
+
+def table_len(wl):
+    return int(max(1, int(wl.positions.max()) + 1))
+
+
+def bench_workload(wl, steps, warmup, stream, with_control=True):
+    from paper_2606_13126_amd.runner import DeviceBatch
+    db = DeviceBatch(wl, table_positions=table_len(wl))
+    db.write()
+    torch.cuda.synchronize()
+    out = {"workload": wl.name}
+    ms = timed(db.attend, steps, warmup, stream)
+    out["attn_ms_median"] = float(np.median(ms))
+    out["attn_ms_p10"] = float(np.percentile(ms, 10))
+    out["attn_ms_p90"] = float(np.percentile(ms, 90))
+    if wl.is_decode:
+        gbs = decode_bytes(wl) / (out["attn_ms_median"] * 1e-3) / 1e9
+        out["decode_GBps"] = gbs
+        out["pct_hbm_peak"] = 100.0 * gbs / PEAK_HBM_GBS
+        out["tokens_per_s"] = wl.num_reqs / (out["attn_ms_median"] * 1e-3)
+    else:
+        tf = flops_of(wl) / (out["attn_ms_median"] * 1e-3) / 1e12
+        out["TFLOPs"] = tf
+        out["pct_bf16_peak"] = 100.0 * tf / PEAK_BF16_TFLOPS
+        out["query_tokens_per_s"] = wl.q.shape[0] / (out["attn_ms_median"] * 1e-3)
+    # computed cos/sin instead of the table
+    nt = DeviceBatch(wl, table_positions=None)
+    nt.k_pool, nt.v_pool = db.k_pool, db.v_pool
+    out["attn_ms_computed_cossin"] = float(np.median(timed(nt.attend, steps, warmup, stream)))
+    if with_control:
+        # same kernel, no RoPE (the pool is read as if it held rotated keys); ABAB timing
+        ctl = DeviceBatch(wl, k_prerotated=True, table_positions=None)
+        ctl.k_pool, ctl.v_pool = db.k_pool, db.v_pool
+        a_ms, b_ms = [], []
+        for _ in range(4):
+            a_ms.append(np.median(timed(db.attend, max(steps // 4, 5), 3, stream)))
+            b_ms.append(np.median(timed(ctl.attend, max(steps // 4, 5), 3, stream)))
+        out["attn_ms_fused_rope"] = float(np.median(a_ms))
+        out["attn_ms_prerotated"] = float(np.median(b_ms))
+        out["rope_overhead_pct"] = 100.0 * (out["attn_ms_fused_rope"] / out["attn_ms_prerotated"] - 1.0)
+    del db, nt
+    torch.cuda.empty_cache()
+    return out
+
+
+def cpu_baseline(wl, budget_s=12.0):
+    """The fp64 oracle (kv_write + prefill) on this host, repeated for about budget_s."""
+    from oracle import workload_oracle as WO
+    try:
+        from threadpoolctl import threadpool_info
+        blas = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        blas = None
+    cores = len(os.sched_getaffinity(0))
+    runs, t0 = 0, time.perf_counter()
+    while True:
+        WO.run(wl)
+        runs += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or runs >= 20:
+            break
+    per = el / runs
+    return {"value": flops_of(wl) / per / 1e12, "unit": "TFLOP/s", "cores": int(blas or cores),
+            "kind": "oracle", "host_cores": cores,
+            "sample": f"whole workload (kv_write + prefill of {wl.q.shape[0]} query tokens x {wl.num_q_heads} heads), "
+                      f"{runs} run(s), {per:.3f} s each, fp64 NumPy"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-extra", action="store_true")
+    ap.add_argument("--configs", default="2,3,4")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (use --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("no GPU visible", file=sys.stderr)
+        sys.exit(2)
+    torch.cuda.set_device(0)
+    from paper_2606_13126_amd.runner import DeviceBatch
+    stream = torch.cuda.current_stream()
+
+    wl = W.config1()
+    flops = flops_of(wl)
+    db = DeviceBatch(wl, table_positions=table_len(wl))
+
+    def step():
+        db.write()
+        db.attend()
+
+    ms = timed(step, args.steps, args.warmup, stream)
+    ms_step = float(np.mean(ms))
+    # dominant kernel: the attention call of the step, timed on its own stream
+    attn_ms = timed(db.attend, args.steps, args.warmup, stream)
+    attn_avg = float(np.mean(attn_ms))
+    achieved = flops / (attn_avg * 1e-3) / 1e12
+    result = {
+        "metric": METRIC,
+        "value": flops / (ms_step * 1e-3) / 1e12,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "llama3_8b_rag_prefill: 1 request, 10 cached SSEP spans x 512 + fresh 256-token "
+                               "PDEP query tail (5376 tokens), 32 q / 8 kv heads, head_dim 128, theta 5e5, "
+                               "block 16, bf16",
+                   "step": "pic_kv_write(256 rows) + pic_attn_prefill"},
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                     "kernel": "pic_attn_prefill (prefill_bf16 + split merge)", "avg_ms": attn_avg},
+    }
+    del db
+    torch.cuda.empty_cache()
+    if not args.no_extra:
+        extra = {"config1": bench_workload(wl, args.steps, args.warmup, stream)}
+        for c in [int(x) for x in args.configs.split(",") if x]:
+            w = W.make_config(c)
+            extra[f"config{c}"] = bench_workload(w, max(args.steps // 2, 10), max(args.warmup // 2, 3), stream)
+            print(f"# config{c}: {json.dumps(extra[f'config{c}'])}", file=sys.stderr, flush=True)
+            del w
+        result["extra"] = extra
+    if not args.no_cpu:
+        result["cpu_baseline"] = cpu_baseline(wl)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -203,7 +203,7 @@ void make_launches(const pic_config* c, HostPlan& hp, std::vector<pic::Plan>& la
                 g.part_base = (int32_t)part;
                 part += (int64_t)g.n_rt * c->num_kv_heads * g.n_split;
                 g.merge_base = (int32_t)merge;
-                merge += (int64_t)g.n_rt * c->num_kv_heads;
+                merge += (int64_t)g.n_rt * c->num_kv_heads * (pic::kTileRows / 32);
             }
             p.g[p.n_groups++] = g;
             ++i;

@@ -160,38 +160,66 @@ __device__ __forceinline__ int find_merge_group(const Plan& plan, int bid) {
     return gi;
 }
 
-// Bit-swap of the two 4-key groups in the middle of every 16 keys: the order in
-// which the PV contraction sees the keys a lane holds after QK^T (see below).
-__device__ __forceinline__ int vt_col(int k) {
-    const int g4 = (k >> 2) & 3;
-    return (k & ~15) | ((((g4 & 1) << 1) | (g4 >> 1)) << 2) | (k & 3);
+constexpr int kWaves = kTileRows / 32;   // 8 waves, 2 per SIMD; wave w owns rows [32w, 32w+32)
+constexpr int kThreads = kWaves * 64;
+
+// max over lanes l and l^32 (one VALU permute, no LDS round trip)
+__device__ __forceinline__ float max_xor32(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
+__device__ __forceinline__ float sum_xor32(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
+
+// Transposing LDS read: within each 16-lane group, lane i receives element i%4 of
+// the 8-byte rows that lanes i/4, i/4+4, i/4+8, i/4+12 point at.
+__device__ __forceinline__ s16x4_t lds_read_tr(const uint16_t* p) {
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(uintptr_t)p);
+}
+
+// One thread's share of a K/V tile in flight: 16 elements of one key's K (NeoX: 8
+// from each half; GPT-J: 16 consecutive) and of its V, plus cos/sin of the 8 pairs.
+struct TileRegs {
+    u32x4_t k[2];
+    u32x4_t v[2];
+    float4 cs[4];
+    int32_t pos;
+    bool ok;
+};
 
 // ---------------------------------------------------------------------------------
 // prefill_bf16
 //
-// Workgroup: 4 waves; wave w owns query rows [64w, 64w+64) of the tile as two
-// 32-column blocks.  Per 64-key tile:
-//   LDS ks[64][D]  rotated K (bf16), 16-byte chunks XOR-swizzled by row;
-//   LDS vt[D][64]  V transposed (bf16), key columns in vt_col order, swizzled.
-//   S^T (64 keys x 32 queries per block) = K Q^T with A = K from LDS and B = Q
-//   in registers: after the MFMA, lane l holds query column l%32 and keys
-//   8*(j/4) + 4*(l/32) + j%4 (j = 0..15) of each 32-key half, so row statistics
-//   need one exchange with lane l^32 only.  Those 16 values are exactly the B
-//   operand of O^T = V^T P^T for two 16-key steps once the contraction index is
-//   taken in vt_col order.
+// Workgroup: 8 waves over up to 256 query rows (token x query head of one KV head's
+// group); wave w owns rows [32w, 32w+32) as the 32 columns of its MFMA tiles.
+// Per 64-key tile (double-buffered in LDS, the next tile's global loads in flight
+// while the current one is consumed):
+//   ks[64][D]  rotated K, bf16, 16-byte chunks XOR-swizzled by key;
+//   vs[64][D]  V as stored (bf16), same swizzle.
+//   S^T (64 keys x 32 queries) = K Q^T: A = K from LDS, B = Q in registers.  After
+//   the MFMA lane l holds query l%32 and keys 8*(j/4) + 4*(l/32) + j%4 (j = 0..15) of
+//   each 32-key half, so row statistics need one exchange with lane l^32.  Those 16
+//   probabilities, in that key order, are the B operand of O^T = V^T P^T for two
+//   16-key steps; the matching A operand (32 dims x the same 8 keys per lane) comes
+//   straight from the untransposed V tile through ds_read_b64_tr_b16.
 // ---------------------------------------------------------------------------------
 template <int D, int STYLE, bool ROPE, bool TABLE>
-__global__ void __launch_bounds__(256, 1) prefill_bf16(const Plan plan, const Args a) {
-    constexpr int KD = D / 16;   // 16-wide contraction steps of QK^T
-    constexpr int DB = D / 32;   // 32-row blocks of O^T
-    constexpr int CH = D / 8;    // 16-byte chunks per K row
+__global__ void __launch_bounds__(kThreads, 1) prefill_bf16(const Plan plan, const Args a) {
+    constexpr int KD = D / 16;    // 16-wide contraction steps of QK^T
+    constexpr int DB = D / 32;    // 32-row blocks of O^T
+    constexpr int CH = D / 8;     // 16-byte chunks per row
     constexpr int HALF = D / 2;
-    constexpr int NB = 2;        // 32-query blocks per wave
     constexpr int BN = kTileKeys;
+    constexpr int TPK = D / 16;   // staging threads per key
+    constexpr int NSTAGE = BN * TPK;
 
-    __shared__ __attribute__((aligned(16))) uint16_t ks[BN * D];
-    __shared__ __attribute__((aligned(16))) uint16_t vt[D * BN];
+    __shared__ __attribute__((aligned(16))) uint16_t ks[2][BN * D];
+    __shared__ __attribute__((aligned(16))) uint16_t vs[2][BN * D];
     __shared__ uint64_t fstep[HALF];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -224,28 +252,27 @@ __global__ void __launch_bounds__(256, 1) prefill_bf16(const Plan plan, const Ar
     if (kv_lo >= kv_hi) return;
 
     if (ROPE) {
-        for (int i = tid; i < HALF; i += 256) fstep[i] = rope_phase_step(a.theta, i, D);
-        __syncthreads();
+        for (int i = tid; i < HALF; i += kThreads) fstep[i] = rope_phase_step(a.theta, i, D);
     }
 
     // ---- queries: rotate at their positions, scale by softmax_scale*log2(e), bf16
-    bf16x8_t qb[NB][KD];
-    int row_tok[NB];
-    const int wave_row0 = row_lo + wave * 64;
+    const int wave_row0 = row_lo + wave * 32;
+    const bool wave_live = wave_row0 < row_hi;
     const int wave_tmin = g.tok0 + min(wave_row0, row_hi - 1) / G;
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-        const int row = wave_row0 + nb * 32 + l32;
-        const bool valid = row < row_hi;
-        const int toff = valid ? row / G : 0;
-        const int hl = valid ? row - toff * G : 0;
-        row_tok[nb] = valid ? g.tok0 + toff : t_last;
+    const int row = wave_row0 + l32;
+    const bool row_valid = row < row_hi;
+    const int toff = row_valid ? row / G : 0;
+    const int hl = row_valid ? row - toff * G : 0;
+    const int row_tok = row_valid ? g.tok0 + toff : t_last;
+    bf16x8_t qb[KD];
+    {
+        __syncthreads();  // fstep ready
         const uint16_t* qp = static_cast<const uint16_t*>(a.q) +
                              ((size_t)(g.q_row0 + toff) * a.hq + (size_t)kvh * G + hl) * D;
         u32x4_t raw[KD];
 #pragma unroll
         for (int kd = 0; kd < KD; ++kd)
-            raw[kd] = valid ? *reinterpret_cast<const u32x4_t*>(qp + kd * 16 + 8 * hi) : u32x4_t{0, 0, 0, 0};
+            raw[kd] = row_valid ? *reinterpret_cast<const u32x4_t*>(qp + kd * 16 + 8 * hi) : u32x4_t{0, 0, 0, 0};
         float xf[KD][8];
 #pragma unroll
         for (int kd = 0; kd < KD; ++kd)
@@ -255,7 +282,7 @@ __global__ void __launch_bounds__(256, 1) prefill_bf16(const Plan plan, const Ar
                 xf[kd][2 * m + 1] = bf_hi(raw[kd][m]);
             }
         if (ROPE) {
-            const int32_t pos = valid ? a.positions[g.pos_off + g.tok0 + toff] : 0;
+            const int32_t pos = row_valid ? a.positions[g.pos_off + g.tok0 + toff] : 0;
             if (STYLE == kNeox) {
 #pragma unroll
                 for (int kd = 0; kd < KD / 2; ++kd) {
@@ -288,237 +315,253 @@ __global__ void __launch_bounds__(256, 1) prefill_bf16(const Plan plan, const Ar
 #pragma unroll
             for (int m = 0; m < 4; ++m)
                 w[m] = pack_bf16(xf[kd][2 * m] * a.scale_log2, xf[kd][2 * m + 1] * a.scale_log2);
-            qb[nb][kd] = __builtin_bit_cast(bf16x8_t, w);
+            qb[kd] = __builtin_bit_cast(bf16x8_t, w);
         }
     }
 
-    f32x16_t acc[NB][DB];
-    float m_run[NB], l_run[NB];
+    f32x16_t acc[DB];
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-        m_run[nb] = kNegBig;
-        l_run[nb] = 0.f;
-#pragma unroll
-        for (int db = 0; db < DB; ++db) acc[nb][db] = f32x16_t{};
-    }
+    for (int db = 0; db < DB; ++db) acc[db] = f32x16_t{};
+    float m_run = kNegBig, l_run = 0.f;
 
     const int32_t* btab = a.block_tables + (size_t)g.req * a.max_blocks;
     const uint16_t* kpool = static_cast<const uint16_t*>(a.k_pool);
     const uint16_t* vpool = static_cast<const uint16_t*>(a.v_pool);
 
-    for (int kt = kv_lo & ~(kBlock - 1); kt < kv_hi; kt += BN) {
-        __syncthreads();  // the previous tile is consumed
-        // ---- K tile: gather, rotate at the keys' positions, bf16 into LDS
-        constexpr int KU = BN * (D / 16);
+    // staging role of this thread: key kk of every tile, 16-element slice c
+    const bool stager = tid < NSTAGE;
+    const int kk = tid / TPK, sc = tid - (tid / TPK) * TPK;
+    const int kt0 = kv_lo & ~(kBlock - 1);
+    const int n_tiles = (kv_hi - kt0 + BN - 1) / BN;
+
+    // per-key metadata one tile ahead of the data loads
+    auto load_meta = [&](int t, int& phys, int32_t& pos) {
+        const int j = kt0 + t * BN + kk;
+        phys = 0;
+        pos = 0;
+        if (stager && t < n_tiles && j >= kv_lo && j < kv_hi) {
+            phys = btab[j >> 4];
+            if (ROPE) pos = a.positions[g.pos_off + j];
+        }
+    };
+    auto load_tile = [&](int t, int phys, int32_t pos, TileRegs& r) {
+        const int j = kt0 + t * BN + kk;
+        r.ok = stager && j >= kv_lo && j < kv_hi;
+        r.pos = pos;
+        r.k[0] = r.k[1] = r.v[0] = r.v[1] = u32x4_t{0, 0, 0, 0};
+        if (r.ok) {
+            const size_t row_off = (((size_t)phys * a.hkv + kvh) * kBlock + (j & 15)) * D;
+            const uint16_t* kp = kpool + row_off;
+            if (STYLE == kNeox) {
+                r.k[0] = *reinterpret_cast<const u32x4_t*>(kp + sc * 8);
+                r.k[1] = *reinterpret_cast<const u32x4_t*>(kp + HALF + sc * 8);
+            } else {
+                r.k[0] = *reinterpret_cast<const u32x4_t*>(kp + sc * 16);
+                r.k[1] = *reinterpret_cast<const u32x4_t*>(kp + sc * 16 + 8);
+            }
+            const uint16_t* vp = vpool + row_off + sc * 16;
+            r.v[0] = *reinterpret_cast<const u32x4_t*>(vp);
+            r.v[1] = *reinterpret_cast<const u32x4_t*>(vp + 8);
+            if (ROPE && TABLE && (uint32_t)pos < (uint32_t)a.rope_len) {
+                const float4* tp = reinterpret_cast<const float4*>(a.rope_table + ((size_t)pos * HALF + sc * 8) * 2);
 #pragma unroll
-        for (int u0 = 0; u0 < KU / 256; ++u0) {
-            const int u = tid + u0 * 256;
-            const int kk = u / (D / 16), c = u - kk * (D / 16);
-            const int j = kt + kk;
-            const bool ok = j >= kv_lo && j < kv_hi;
-            u32x4_t xa = {0, 0, 0, 0}, xb = {0, 0, 0, 0};
-            if (ok) {
-                const int phys = btab[j >> 4];
-                const uint16_t* src = kpool + (((size_t)phys * a.hkv + kvh) * kBlock + (j & 15)) * D;
-                if (STYLE == kNeox) {
-                    xa = *reinterpret_cast<const u32x4_t*>(src + c * 8);
-                    xb = *reinterpret_cast<const u32x4_t*>(src + HALF + c * 8);
-                } else {
-                    xa = *reinterpret_cast<const u32x4_t*>(src + c * 16);
-                    xb = *reinterpret_cast<const u32x4_t*>(src + c * 16 + 8);
+                for (int k = 0; k < 4; ++k) r.cs[k] = tp[k];
+            }
+        }
+    };
+    auto store_tile = [&](int buf, TileRegs& r) {
+        if (!stager) return;
+        if (ROPE && r.ok) {
+            float c[8], s[8];
+            if (TABLE && (uint32_t)r.pos < (uint32_t)a.rope_len) {
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    c[2 * k] = r.cs[k].x; s[2 * k] = r.cs[k].y; c[2 * k + 1] = r.cs[k].z; s[2 * k + 1] = r.cs[k].w;
                 }
-                if (ROPE) {
-                    const int32_t pos = a.positions[g.pos_off + j];
-                    float cs[8], sn[8];
-                    rope_cs_n<8, TABLE>(a.rope_table, a.rope_len, HALF, fstep, pos, c * 8, cs, sn);
-                    if (STYLE == kNeox) {
+            } else {
 #pragma unroll
-                        for (int m = 0; m < 4; ++m) {
-                            const float x0 = bf_lo(xa[m]), x1 = bf_hi(xa[m]);
-                            const float y0 = bf_lo(xb[m]), y1 = bf_hi(xb[m]);
-                            const float c0 = cs[2 * m], c1 = cs[2 * m + 1], s0 = sn[2 * m], s1 = sn[2 * m + 1];
-                            xa[m] = pack_bf16(x0 * c0 - y0 * s0, x1 * c1 - y1 * s1);
-                            xb[m] = pack_bf16(y0 * c0 + x0 * s0, y1 * c1 + x1 * s1);
-                        }
-                    } else {
+                for (int k = 0; k < 8; ++k) rope_cs(r.pos, fstep[sc * 8 + k], c[k], s[k]);
+            }
+            if (STYLE == kNeox) {
 #pragma unroll
-                        for (int m = 0; m < 4; ++m) {
-                            const float x0 = bf_lo(xa[m]), y0 = bf_hi(xa[m]);
-                            xa[m] = pack_bf16(x0 * cs[m] - y0 * sn[m], y0 * cs[m] + x0 * sn[m]);
-                            const float x1 = bf_lo(xb[m]), y1 = bf_hi(xb[m]);
-                            xb[m] = pack_bf16(x1 * cs[4 + m] - y1 * sn[4 + m], y1 * cs[4 + m] + x1 * sn[4 + m]);
-                        }
+                for (int m = 0; m < 4; ++m) {
+                    const float x0 = bf_lo(r.k[0][m]), x1 = bf_hi(r.k[0][m]);
+                    const float y0 = bf_lo(r.k[1][m]), y1 = bf_hi(r.k[1][m]);
+                    const float c0 = c[2 * m], c1 = c[2 * m + 1], s0 = s[2 * m], s1 = s[2 * m + 1];
+                    r.k[0][m] = pack_bf16(x0 * c0 - y0 * s0, x1 * c1 - y1 * s1);
+                    r.k[1][m] = pack_bf16(y0 * c0 + x0 * s0, y1 * c1 + x1 * s1);
+                }
+            } else {
+#pragma unroll
+                for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+                    for (int m = 0; m < 4; ++m) {
+                        const float x = bf_lo(r.k[h2][m]), y = bf_hi(r.k[h2][m]);
+                        const float cc = c[4 * h2 + m], ss = s[4 * h2 + m];
+                        r.k[h2][m] = pack_bf16(x * cc - y * ss, y * cc + x * ss);
                     }
-                }
-            }
-            const int ca = STYLE == kNeox ? c : 2 * c;
-            const int cb = STYLE == kNeox ? c + CH / 2 : 2 * c + 1;
-            const int sw = kk & (CH - 1);
-            *reinterpret_cast<u32x4_t*>(ks + kk * D + ((ca ^ sw) << 3)) = xa;
-            *reinterpret_cast<u32x4_t*>(ks + kk * D + ((cb ^ sw) << 3)) = xb;
-        }
-        // ---- V tile: gather 4 keys x 8 dims per thread, transpose into vt
-        constexpr int VU = (BN / 4) * CH;
-        if (tid < VU) {
-            const int kg = tid / CH, dc = tid - kg * CH;
-            u32x4_t r[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int j = kt + kg * 4 + e;
-                r[e] = u32x4_t{0, 0, 0, 0};
-                if (j >= kv_lo && j < kv_hi) {
-                    const int phys = btab[j >> 4];
-                    r[e] = *reinterpret_cast<const u32x4_t*>(
-                        vpool + (((size_t)phys * a.hkv + kvh) * kBlock + (j & 15)) * D + dc * 8);
-                }
-            }
-            const int col = vt_col(kg * 4);
-#pragma unroll
-            for (int m = 0; m < 4; ++m) {
-                const u32x2_t lo = {(r[0][m] & 0xffffu) | (r[1][m] << 16), (r[2][m] & 0xffffu) | (r[3][m] << 16)};
-                const u32x2_t hv = {(r[0][m] >> 16) | (r[1][m] & 0xffff0000u),
-                                    (r[2][m] >> 16) | (r[3][m] & 0xffff0000u)};
-                const int d0 = dc * 8 + 2 * m, d1 = d0 + 1;
-                *reinterpret_cast<u32x2_t*>(vt + d0 * BN + ((((col >> 3) ^ (d0 & 7)) << 3) | (col & 7))) = lo;
-                *reinterpret_cast<u32x2_t*>(vt + d1 * BN + ((((col >> 3) ^ (d1 & 7)) << 3) | (col & 7))) = hv;
             }
         }
-        __syncthreads();
+        const int sw = kk & (CH - 1);
+        uint16_t* krow = &ks[buf][kk * D];
+        uint16_t* vrow = &vs[buf][kk * D];
+        const int ca = STYLE == kNeox ? sc : 2 * sc;
+        const int cb = STYLE == kNeox ? sc + CH / 2 : 2 * sc + 1;
+        *reinterpret_cast<u32x4_t*>(krow + ((ca ^ sw) << 3)) = r.k[0];
+        *reinterpret_cast<u32x4_t*>(krow + ((cb ^ sw) << 3)) = r.k[1];
+        *reinterpret_cast<u32x4_t*>(vrow + (((2 * sc) ^ sw) << 3)) = r.v[0];
+        *reinterpret_cast<u32x4_t*>(vrow + (((2 * sc + 1) ^ sw) << 3)) = r.v[1];
+    };
 
-        // ---- S^T = K Q^T
-        f32x16_t s[NB][2];
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) s[nb][0] = s[nb][1] = f32x16_t{};
-#pragma unroll
-        for (int mb = 0; mb < 2; ++mb) {
-            const int kr = mb * 32 + l32;
-#pragma unroll
-            for (int kd = 0; kd < KD; ++kd) {
-                const bf16x8_t af = *reinterpret_cast<const bf16x8_t*>(
-                    ks + kr * D + (((kd * 2 + hi) ^ (kr & (CH - 1))) << 3));
-#pragma unroll
-                for (int nb = 0; nb < NB; ++nb)
-                    s[nb][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, qb[nb][kd], s[nb][mb], 0, 0, 0);
-            }
-        }
+    TileRegs regs;
+    int phys_n, phys_nn;
+    int32_t pos_n, pos_nn;
+    load_meta(0, phys_n, pos_n);
+    load_tile(0, phys_n, pos_n, regs);
+    load_meta(1, phys_nn, pos_nn);
+    store_tile(0, regs);
+    __syncthreads();
 
-        // ---- window mask (only on tiles that cross a boundary of the visible set)
-        const bool need_mask = kt < kv_lo || kt + BN > kv_hi || kt + BN - 1 > wave_tmin;
-        if (need_mask) {
+    for (int t = 0; t < n_tiles; ++t) {
+        const int buf = t & 1;
+        const int kt = kt0 + t * BN;
+        const bool more = t + 1 < n_tiles;
+        if (more) {
+            load_tile(t + 1, phys_nn, pos_nn, regs);
+            load_meta(t + 2, phys_nn, pos_nn);
+        }
+        if (wave_live) {
+            // ---- S^T = K Q^T
+            f32x16_t s[2] = {f32x16_t{}, f32x16_t{}};
 #pragma unroll
-            for (int nb = 0; nb < NB; ++nb)
+            for (int kd = 0; kd < KD; ++kd)
+#pragma unroll
+                for (int mb = 0; mb < 2; ++mb) {
+                    const int kr = mb * 32 + l32;
+                    const bf16x8_t af = *reinterpret_cast<const bf16x8_t*>(
+                        &ks[buf][kr * D + (((kd * 2 + hi) ^ (kr & (CH - 1))) << 3)]);
+                    s[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, qb[kd], s[mb], 0, 0, 0);
+                }
+            // ---- window mask, only on tiles that cross a boundary of the visible set
+            if (kt < kv_lo || kt + BN > kv_hi || kt + BN - 1 > wave_tmin) {
 #pragma unroll
                 for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
                     for (int j = 0; j < 16; ++j) {
                         const int key = kt + mb * 32 + 8 * (j >> 2) + 4 * hi + (j & 3);
-                        if (key < kv_lo || key >= kv_hi || key > row_tok[nb]) s[nb][mb][j] = -INFINITY;
+                        if (key < kv_lo || key >= kv_hi || key > row_tok) s[mb][j] = -INFINITY;
                     }
-        }
-
-        // ---- online softmax (log2 domain)
-        bf16x8_t pb[NB][2][2];
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
+            }
+            // ---- online softmax in the log2 domain.  The reference maximum only moves
+            // when some row's maximum grows by more than 8 (probabilities stay below 2^8),
+            // so most tiles skip rescaling the accumulators.
             float mx = kNegBig;
 #pragma unroll
             for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-                for (int j = 0; j < 16; ++j) mx = fmaxf(mx, s[nb][mb][j]);
-            mx = fmaxf(mx, __shfl_xor(mx, 32));
-            const float m_new = fmaxf(m_run[nb], mx);
-            const float alpha = __builtin_amdgcn_exp2f(m_run[nb] - m_new);
-            float ls = 0.f;
+                for (int j = 0; j < 16; ++j) mx = fmaxf(mx, s[mb][j]);
+            mx = max_xor32(mx);
+            if (__builtin_amdgcn_ballot_w64(mx > m_run + 8.f) != 0) {
+                const float m_new = fmaxf(m_run, mx);
+                const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+                l_run *= alpha;
+#pragma unroll
+                for (int db = 0; db < DB; ++db) acc[db] *= alpha;
+                m_run = m_new;
+            }
+            bf16x8_t pb[2][2];
 #pragma unroll
             for (int mb = 0; mb < 2; ++mb) {
 #pragma unroll
                 for (int j = 0; j < 16; ++j) {
-                    const float p = __builtin_amdgcn_exp2f(s[nb][mb][j] - m_new);
-                    s[nb][mb][j] = p;
-                    ls += p;
+                    const float p = __builtin_amdgcn_exp2f(s[mb][j] - m_run);
+                    s[mb][j] = p;
+                    l_run += p;
                 }
 #pragma unroll
-                for (int ks2 = 0; ks2 < 2; ++ks2) {
+                for (int k2 = 0; k2 < 2; ++k2) {
                     u32x4_t w;
 #pragma unroll
-                    for (int m = 0; m < 4; ++m)
-                        w[m] = pack_bf16(s[nb][mb][8 * ks2 + 2 * m], s[nb][mb][8 * ks2 + 2 * m + 1]);
-                    pb[nb][mb][ks2] = __builtin_bit_cast(bf16x8_t, w);
+                    for (int m = 0; m < 4; ++m) w[m] = pack_bf16(s[mb][8 * k2 + 2 * m], s[mb][8 * k2 + 2 * m + 1]);
+                    pb[mb][k2] = __builtin_bit_cast(bf16x8_t, w);
                 }
             }
-            l_run[nb] = l_run[nb] * alpha + ls;
-            m_run[nb] = m_new;
+            // ---- O^T += V^T P^T; the A operand rows are dims, its 8 keys per lane are
+            // keys 16*k2 + 4*(l/32) + {0..3} and the same + 8 of each 32-key half
+            const int q16 = (lane >> 4) & 1;
+            const int kq = (lane & 15) >> 2;
+            const int dq = 4 * (lane & 3);
 #pragma unroll
-            for (int db = 0; db < DB; ++db) acc[nb][db] *= alpha;
+            for (int db = 0; db < DB; ++db) {
+                const int d = db * 32 + q16 * 16 + dq;
+#pragma unroll
+                for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+                    for (int k2 = 0; k2 < 2; ++k2) {
+                        const int key0 = mb * 32 + 16 * k2 + 4 * hi + kq;
+                        const int key1 = key0 + 8;
+                        const s16x4_t lo = lds_read_tr(
+                            &vs[buf][key0 * D + (((d >> 3) ^ (key0 & (CH - 1))) << 3) + (d & 7)]);
+                        const s16x4_t up = lds_read_tr(
+                            &vs[buf][key1 * D + (((d >> 3) ^ (key1 & (CH - 1))) << 3) + (d & 7)]);
+                        const s16x4_t both[2] = {lo, up};
+                        const bf16x8_t af = __builtin_bit_cast(bf16x8_t, both);
+                        acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, pb[mb][k2], acc[db], 0, 0, 0);
+                    }
+            }
         }
-
-        // ---- O^T += V^T P^T
-#pragma unroll
-        for (int db = 0; db < DB; ++db) {
-            const int dr = db * 32 + l32;
-#pragma unroll
-            for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-                for (int ks2 = 0; ks2 < 2; ++ks2) {
-                    const int chunk = mb * 4 + ks2 * 2 + hi;
-                    const bf16x8_t af = *reinterpret_cast<const bf16x8_t*>(vt + dr * BN + ((chunk ^ (dr & 7)) << 3));
-#pragma unroll
-                    for (int nb = 0; nb < NB; ++nb)
-                        acc[nb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, pb[nb][mb][ks2], acc[nb][db], 0, 0, 0);
-                }
-        }
+        if (more) store_tile(buf ^ 1, regs);
+        __syncthreads();
     }
 
     // ---- epilogue: normalise and store, or store the split's partial state
+    const float lt = sum_xor32(l_run);
+    if (!row_valid) return;
+    if (g.n_split == 1) {
+        const float inv = 1.f / lt;
+        uint16_t* op = static_cast<uint16_t*>(a.o) + ((size_t)(g.q_row0 + toff) * a.hq + (size_t)kvh * G + hl) * D;
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-        const float lt = l_run[nb] + __shfl_xor(l_run[nb], 32);
-        const int row = wave_row0 + nb * 32 + l32;
-        if (row >= row_hi) continue;
-        if (g.n_split == 1) {
-            const float inv = 1.f / lt;
-            const int toff = row / G, hl = row - toff * G;
-            uint16_t* op = static_cast<uint16_t*>(a.o) + ((size_t)(g.q_row0 + toff) * a.hq + (size_t)kvh * G + hl) * D;
+        for (int db = 0; db < DB; ++db)
 #pragma unroll
-            for (int db = 0; db < DB; ++db)
+            for (int q4 = 0; q4 < 4; ++q4) {
+                const int d = db * 32 + 8 * q4 + 4 * hi;
+                const u32x2_t w = {pack_bf16(acc[db][4 * q4] * inv, acc[db][4 * q4 + 1] * inv),
+                                   pack_bf16(acc[db][4 * q4 + 2] * inv, acc[db][4 * q4 + 3] * inv)};
+                *reinterpret_cast<u32x2_t*>(op + d) = w;
+            }
+    } else {
+        const size_t slot = (size_t)g.part_base + (size_t)cluster * g.n_rt + rt;
+        float* po = a.part_o + (slot * kTileRows + (row - row_lo)) * D;
 #pragma unroll
-                for (int q4 = 0; q4 < 4; ++q4) {
-                    const int d = db * 32 + 8 * q4 + 4 * hi;
-                    const u32x2_t w = {pack_bf16(acc[nb][db][4 * q4] * inv, acc[nb][db][4 * q4 + 1] * inv),
-                                       pack_bf16(acc[nb][db][4 * q4 + 2] * inv, acc[nb][db][4 * q4 + 3] * inv)};
-                    *reinterpret_cast<u32x2_t*>(op + d) = w;
-                }
-        } else {
-            const size_t slot = (size_t)g.part_base + (size_t)cluster * g.n_rt + rt;
-            float* po = a.part_o + (slot * kTileRows + (row - row_lo)) * D;
+        for (int db = 0; db < DB; ++db)
 #pragma unroll
-            for (int db = 0; db < DB; ++db)
-#pragma unroll
-                for (int q4 = 0; q4 < 4; ++q4) {
-                    const int d = db * 32 + 8 * q4 + 4 * hi;
-                    *reinterpret_cast<float4*>(po + d) =
-                        make_float4(acc[nb][db][4 * q4], acc[nb][db][4 * q4 + 1], acc[nb][db][4 * q4 + 2],
-                                    acc[nb][db][4 * q4 + 3]);
-                }
-            if (hi == 0)
-                *reinterpret_cast<float2*>(a.part_ml + (slot * kTileRows + (row - row_lo)) * 2) =
-                    make_float2(m_run[nb], lt);
-        }
+            for (int q4 = 0; q4 < 4; ++q4) {
+                const int d = db * 32 + 8 * q4 + 4 * hi;
+                *reinterpret_cast<float4*>(po + d) =
+                    make_float4(acc[db][4 * q4], acc[db][4 * q4 + 1], acc[db][4 * q4 + 2], acc[db][4 * q4 + 3]);
+            }
+        if (hi == 0)
+            *reinterpret_cast<float2*>(a.part_ml + (slot * kTileRows + (row - row_lo)) * 2) = make_float2(m_run, lt);
     }
 }
 
 // ---------------------------------------------------------------------------------
 // merge: O = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s over the non-empty splits
-// of one (row tile, KV head); one block per pair.
+// of one (row tile, KV head); one block per 32 rows, 8 threads per row.
 // ---------------------------------------------------------------------------------
-template <int D, typename TO>
+constexpr int kMergeRows = 32;
+
+template <int D>
 __global__ void __launch_bounds__(256) merge_kernel(const Plan plan, const Args a) {
     const int gi = find_merge_group(plan, blockIdx.x);
     if (gi < 0) return;
     const Group g = plan.g[gi];
-    const int li = blockIdx.x - g.merge_base;
-    if (li >= a.hkv * g.n_rt) return;
-    const int kvh = li / g.n_rt, rt = li - kvh * g.n_rt;
+    constexpr int CHUNKS = kTileRows / kMergeRows;
+    int li = blockIdx.x - g.merge_base;
+    if (li >= a.hkv * g.n_rt * CHUNKS) return;
+    const int chunk = li % CHUNKS;
+    li /= CHUNKS;
+    const int kvh = li / g.n_rt, rt = li - (li / g.n_rt) * g.n_rt;
     const int G = a.group;
     const int row_lo = rt * kTileRows;
     const int row_hi = min(row_lo + kTileRows, g.n_tok * G);
@@ -526,35 +569,40 @@ __global__ void __launch_bounds__(256) merge_kernel(const Plan plan, const Args 
     int n_live = 0;
     for (int s = 0; s < g.n_split; ++s)
         if (g.win + s * g.split_keys < t_last + 1) n_live = s + 1;
-    constexpr int Q4 = D / 4;
-    for (int u = threadIdx.x; u < (row_hi - row_lo) * Q4; u += blockDim.x) {
-        const int r = u / Q4, q4 = u - r * Q4;
-        float mmax = kNegBig;
-        for (int s = 0; s < n_live; ++s) {
-            const size_t slot = (size_t)g.part_base + ((size_t)kvh * g.n_split + s) * g.n_rt + rt;
-            const float2 ml = *reinterpret_cast<const float2*>(a.part_ml + (slot * kTileRows + r) * 2);
-            if (ml.y > 0.f) mmax = fmaxf(mmax, ml.x);
-        }
-        float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
-        float den = 0.f;
-        for (int s = 0; s < n_live; ++s) {
-            const size_t slot = (size_t)g.part_base + ((size_t)kvh * g.n_split + s) * g.n_rt + rt;
-            const float2 ml = *reinterpret_cast<const float2*>(a.part_ml + (slot * kTileRows + r) * 2);
-            if (!(ml.y > 0.f)) continue;
-            const float w = __builtin_amdgcn_exp2f(ml.x - mmax);
-            const float4 v = *reinterpret_cast<const float4*>(a.part_o + (slot * kTileRows + r) * D + q4 * 4);
-            num.x += w * v.x; num.y += w * v.y; num.z += w * v.z; num.w += w * v.w;
-            den += w * ml.y;
-        }
-        const float inv = 1.f / den;
-        const int row = row_lo + r;
-        const int toff = row / G, hl = row - toff * G;
-        TO* op = static_cast<TO*>(a.o) + ((size_t)(g.q_row0 + toff) * a.hq + (size_t)kvh * G + hl) * D + q4 * 4;
-        op[0] = (TO)(num.x * inv);
-        op[1] = (TO)(num.y * inv);
-        op[2] = (TO)(num.z * inv);
-        op[3] = (TO)(num.w * inv);
+    const int r = chunk * kMergeRows + (int)threadIdx.x / 8;
+    if (row_lo + r >= row_hi) return;
+    constexpr int PER = D / 8;   // floats per thread
+    const int d0 = ((int)threadIdx.x & 7) * PER;
+    float mmax = kNegBig;
+    for (int s = 0; s < n_live; ++s) {
+        const size_t slot = (size_t)g.part_base + ((size_t)kvh * g.n_split + s) * g.n_rt + rt;
+        const float2 ml = *reinterpret_cast<const float2*>(a.part_ml + (slot * kTileRows + r) * 2);
+        if (ml.y > 0.f) mmax = fmaxf(mmax, ml.x);
     }
+    float num[PER];
+#pragma unroll
+    for (int e = 0; e < PER; ++e) num[e] = 0.f;
+    float den = 0.f;
+    for (int s = 0; s < n_live; ++s) {
+        const size_t slot = (size_t)g.part_base + ((size_t)kvh * g.n_split + s) * g.n_rt + rt;
+        const float2 ml = *reinterpret_cast<const float2*>(a.part_ml + (slot * kTileRows + r) * 2);
+        if (!(ml.y > 0.f)) continue;
+        const float w = __builtin_amdgcn_exp2f(ml.x - mmax);
+        const float4* v = reinterpret_cast<const float4*>(a.part_o + (slot * kTileRows + r) * D + d0);
+#pragma unroll
+        for (int e = 0; e < PER / 4; ++e) {
+            const float4 x = v[e];
+            num[4 * e] += w * x.x; num[4 * e + 1] += w * x.y; num[4 * e + 2] += w * x.z; num[4 * e + 3] += w * x.w;
+        }
+        den += w * ml.y;
+    }
+    const float inv = 1.f / den;
+    const int row = row_lo + r;
+    const int toff = row / G, hl = row - toff * G;
+    uint32_t* op = reinterpret_cast<uint32_t*>(static_cast<uint16_t*>(a.o) +
+                                               ((size_t)(g.q_row0 + toff) * a.hq + (size_t)kvh * G + hl) * D + d0);
+#pragma unroll
+    for (int e = 0; e < PER / 2; ++e) op[e] = pack_bf16(num[2 * e] * inv, num[2 * e + 1] * inv);
 }
 
 // ---------------------------------------------------------------------------------
@@ -649,11 +697,11 @@ hipError_t launch_attn_t(int dtype, const Plan& plan, const Args& a, hipStream_t
         hipLaunchKernelGGL((attn_f32<D, STYLE, ROPE, TABLE>), dim3(plan.n_items), dim3(64), 0, st, plan, a);
         return hipGetLastError();
     }
-    hipLaunchKernelGGL((prefill_bf16<D, STYLE, ROPE, TABLE>), dim3(plan.n_items), dim3(256), 0, st, plan, a);
+    hipLaunchKernelGGL((prefill_bf16<D, STYLE, ROPE, TABLE>), dim3(plan.n_items), dim3(kThreads), 0, st, plan, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (plan.n_merge > 0) {
-        hipLaunchKernelGGL((merge_kernel<D, __bf16>), dim3(plan.n_merge), dim3(256), 0, st, plan, a);
+        hipLaunchKernelGGL((merge_kernel<D>), dim3(plan.n_merge), dim3(256), 0, st, plan, a);
         e = hipGetLastError();
     }
     return e;
