@@ -100,13 +100,15 @@ typedef struct pic_batch_dev {
     const int32_t* positions;    /* DEVICE [sum L_r], any int32 values */
 } pic_batch_dev;
 
-/* Optional cos/sin table (the paper's cos_sin lookup, Sec. 3.2.2): entry
- * [p][i] = (cos(p*omega_i), sin(p*omega_i)) as two float32, for p in [0, len).
- * Built by pic_rope_table_build.  Positions outside [0, len), and every position
- * when data is NULL, are rotated with cos/sin computed in the kernel from an exact
- * fixed-point phase. */
+/* Optional cos/sin table (the paper's cos_sin lookup, Sec. 3.2.2): one 8-byte entry
+ * per (position p in [0, len), pair i in [0, D/2)), from cos/sin(p*omega_i) computed
+ * in float64.  PIC_F32 tables hold (cos, sin) as two float32; PIC_BF16 tables hold
+ * (cos, -sin, sin, cos) as four bf16, so that the kernel rotates a pair (x, y) with
+ * two 2-element dot products.  Built by pic_rope_table_build for cfg->dtype.
+ * Positions outside [0, len), and every position when data is NULL, are rotated
+ * with cos/sin computed in the kernel from an exact fixed-point phase. */
 typedef struct pic_rope_table {
-    const void* data; /* DEVICE [len][D/2][2] float32, or NULL */
+    const void* data; /* DEVICE [len][D/2] 8-byte entries, or NULL */
     int32_t len;
 } pic_rope_table;
 
@@ -119,8 +121,8 @@ const char* pic_last_error(void);
 /* Bytes of the cos/sin table for positions [0, num_positions). */
 pic_status pic_rope_table_bytes(const pic_config* cfg, int32_t num_positions, size_t* bytes);
 
-/* Fill `table` (DEVICE, pic_rope_table_bytes bytes) with cos/sin of p*omega_i for
- * p in [0, num_positions), computed in float64 and rounded to float32. */
+/* Fill `table` (DEVICE, pic_rope_table_bytes bytes) with the entries of positions
+ * [0, num_positions) in the format of cfg->dtype (see pic_rope_table). */
 pic_status pic_rope_table_build(const pic_config* cfg, int32_t num_positions, void* table, void* stream);
 
 /* Rotate x (DEVICE [n][num_heads][D], cfg->dtype) in place by R_p with

@@ -299,7 +299,7 @@ pic_status pic_rope_table_build(const pic_config* cfg, int32_t num_positions, vo
     if (st) return st;
     if (num_positions < 0) return fail(PIC_EINVAL, "num_positions < 0");
     if (num_positions > 0 && table == nullptr) return fail(PIC_EINVAL, "table is NULL");
-    return hip_status(pic::launch_rope_table(cfg->head_dim, cfg->rope_theta, num_positions,
+    return hip_status(pic::launch_rope_table(cfg->dtype, cfg->head_dim, cfg->rope_theta, num_positions,
                                              static_cast<float*>(table), stream),
                       "rope table launch");
 }

@@ -46,7 +46,7 @@ struct Args {
     const void* v_pool;
     const int32_t* block_tables;
     const int32_t* positions;
-    const float* rope_table;  // [rope_len][D/2][2] or null
+    const float* rope_table;  // [rope_len][D/2] 8-byte entries (format by dtype) or null
     float* part_o;            // [slot][kTileRows][D] unnormalised partial outputs
     float* part_ml;           // [slot][kTileRows][2] running max (log2 units) and sum
     double theta;
@@ -61,7 +61,7 @@ struct Args {
 // Launchers implemented in pic_kernels.hip.  Each returns a hipError_t value.
 int launch_kv_write(int dtype, int hkv, int d, void* k_pool, void* v_pool, const void* k_new,
                     const void* v_new, const int32_t* slots, int n, void* stream);
-int launch_rope_table(int d, double theta, int n_pos, float* table, void* stream);
+int launch_rope_table(int dtype, int d, double theta, int n_pos, float* table, void* stream);
 int launch_rope_rotate(int dtype, int style, int d, double theta, const float* table, int rope_len, void* x,
                        int n, int heads, const int32_t* positions, void* stream);
 int launch_attention(int dtype, int style, int d, bool rope, const Plan& plan, const Args& args, void* stream);

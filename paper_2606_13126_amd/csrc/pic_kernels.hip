@@ -18,6 +18,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "pic_internal.h"
 
 namespace pic {
@@ -27,6 +29,7 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 
 constexpr int kNeox = 0;
 constexpr float kNegBig = -1.0e30f;  // finite "minus infinity" for running maxima
@@ -35,9 +38,14 @@ constexpr double kInv2Pi = 0.15915494309189533577;
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
+// (a.lo * b.lo + a.hi * b.hi) of two bf16 pairs, fp32 result.
+__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b) {
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a), __builtin_bit_cast(bf16x2_t, b), 0.0f,
+                                           false);
+}
+
 // Round two floats to bf16 (round to nearest even) and pack them, lo first.
 __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
-    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
     bf16x2_t v = {(__bf16)lo, (__bf16)hi};
     return __builtin_bit_cast(uint32_t, v);
 }
@@ -67,17 +75,27 @@ __device__ __forceinline__ void rope_cs_f64(int32_t pos, uint64_t step, double& 
     sincospi(2.0 * r, &s, &c);
 }
 
-// cos/sin of N consecutive frequencies i0 .. i0+N-1 at position pos: from the table
-// when pos is inside it, else computed.
+// Table entries: float32 kernels read (cos, sin) as two floats; bf16 kernels read
+// (cos, -sin) and (sin, cos) as two bf16 pairs, so that rotating a pair (x, y) is
+// two 2-element dot products: x' = (x, y).(c, -s), y' = (x, y).(s, c).
+__device__ __forceinline__ void cs_from_bf16_entry(uint2 w, float& c, float& s) {
+    c = bf_lo(w.x);
+    s = bf_lo(w.y);
+}
+__device__ __forceinline__ uint2 bf16_entry(float c, float s) { return make_uint2(pack_bf16(c, -s), pack_bf16(s, c)); }
+
+// cos/sin of N consecutive frequencies i0 .. i0+N-1 at position pos from a bf16
+// table when pos is inside it, else computed.
 template <int N, bool TABLE>
 __device__ __forceinline__ void rope_cs_n(const float* __restrict__ table, int rope_len, int half,
                                           const uint64_t* fstep, int32_t pos, int i0, float* c, float* s) {
     if (TABLE && (uint32_t)pos < (uint32_t)rope_len) {
-        const float4* t = reinterpret_cast<const float4*>(table + ((size_t)pos * half + i0) * 2);
+        const uint4* t = reinterpret_cast<const uint4*>(table + ((size_t)pos * half + i0) * 2);
 #pragma unroll
         for (int k = 0; k < N / 2; ++k) {
-            const float4 v = t[k];
-            c[2 * k] = v.x; s[2 * k] = v.y; c[2 * k + 1] = v.z; s[2 * k + 1] = v.w;
+            const uint4 v = t[k];
+            cs_from_bf16_entry(make_uint2(v.x, v.y), c[2 * k], s[2 * k]);
+            cs_from_bf16_entry(make_uint2(v.z, v.w), c[2 * k + 1], s[2 * k + 1]);
         }
     } else {
 #pragma unroll
@@ -107,16 +125,18 @@ __global__ void __launch_bounds__(256) kv_write_kernel(u32x4_t* __restrict__ k_p
 }
 
 // ---------------------------------------------------------------------------------
-// rope_table: entry [p][i] = (cos, sin)(p * omega_i), float64 math, float32 storage.
+// rope_table: entry [p][i] from cos/sin(p * omega_i) in float64, stored as float32
+// (cos, sin) or as bf16 (cos, -sin, sin, cos).
 // ---------------------------------------------------------------------------------
-__global__ void __launch_bounds__(256) rope_table_kernel(float2* __restrict__ table, int n_pos, int half, int d,
-                                                         double theta) {
+__global__ void __launch_bounds__(256) rope_table_kernel(uint2* __restrict__ table, int n_pos, int half, int d,
+                                                         double theta, bool bf16_pairs) {
     const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (idx >= (int64_t)n_pos * half) return;
     const int p = (int)(idx / half), i = (int)(idx - (int64_t)p * half);
     double c, s;
     rope_cs_f64(p, rope_phase_step(theta, i, d), c, s);
-    table[idx] = make_float2((float)c, (float)s);
+    table[idx] = bf16_pairs ? bf16_entry((float)c, (float)s)
+                            : make_uint2(__float_as_uint((float)c), __float_as_uint((float)s));
 }
 
 // ---------------------------------------------------------------------------------
@@ -125,7 +145,7 @@ __global__ void __launch_bounds__(256) rope_table_kernel(float2* __restrict__ ta
 template <typename T, int STYLE>
 __global__ void __launch_bounds__(256) rope_rotate_kernel(T* __restrict__ x, int64_t n_pairs, int heads, int d,
                                                           double theta, const int32_t* __restrict__ positions,
-                                                          const float2* __restrict__ table, int rope_len) {
+                                                          const uint2* __restrict__ table, int rope_len) {
     const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (idx >= n_pairs) return;
     const int half = d / 2;
@@ -134,8 +154,13 @@ __global__ void __launch_bounds__(256) rope_rotate_kernel(T* __restrict__ x, int
     const int32_t pos = positions[rh / heads];
     float c, s;
     if (table != nullptr && (uint32_t)pos < (uint32_t)rope_len) {
-        const float2 v = table[(size_t)pos * half + i];
-        c = v.x; s = v.y;
+        const uint2 v = table[(size_t)pos * half + i];
+        if (sizeof(T) == 4) {
+            c = __uint_as_float(v.x);
+            s = __uint_as_float(v.y);
+        } else {
+            cs_from_bf16_entry(v, c, s);
+        }
     } else {
         rope_cs(pos, rope_phase_step(theta, i, d), c, s);
     }
@@ -176,21 +201,48 @@ __device__ __forceinline__ float sum_xor32(float x) {
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
 
-// Transposing LDS read: within each 16-lane group, lane i receives element i%4 of
-// the 8-byte rows that lanes i/4, i/4+4, i/4+8, i/4+12 point at.
-__device__ __forceinline__ s16x4_t lds_read_tr(const uint16_t* p) {
-    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(uintptr_t)p);
+// XOR swizzle of the 16-byte chunks of LDS row `key`.  D = 128: 16 consecutive keys
+// get 16 different patterns (conflict-free K operand reads) and 4 consecutive keys
+// land in 4 different aligned groups of 4 chunks (conflict-free transposing V reads).
+// D = 64 (two rows per bank line): 16 consecutive keys cover both halves x 8 chunks.
+template <int D>
+__device__ __forceinline__ int swz(int key) {
+    if (D == 128) return ((key & 3) << 2) | ((key >> 2) & 3);
+    return (key >> 1) & 7;
 }
 
-// One thread's share of a K/V tile in flight: 16 elements of one key's K (NeoX: 8
-// from each half; GPT-J: 16 consecutive) and of its V, plus cos/sin of the 8 pairs.
+typedef __attribute__((address_space(3))) const uint16_t lds_u16_t;
+
+// an LDS array element as an LDS-space pointer (constant offsets then fold into
+// the instruction's offset field)
+__device__ __forceinline__ lds_u16_t* as_lds(const uint16_t* p) { return (lds_u16_t*)p; }
+
+// Transposing LDS read: within each 16-lane group, lane i receives element i%4 of
+// the 8-byte rows that lanes i/4, i/4+4, i/4+8, i/4+12 point at.
+__device__ __forceinline__ s16x4_t lds_read_tr(lds_u16_t* p) {
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)p);
+}
+
+// One thread's share of a K tile in flight when K is rotated on its way to LDS:
+// 16 elements of one key (NeoX: 8 from each half; GPT-J: 16 consecutive) and the
+// table entries of their 8 pairs.
 struct TileRegs {
     u32x4_t k[2];
-    u32x4_t v[2];
     float4 cs[4];
     int32_t pos;
     bool ok;
 };
+
+// wait until this wave's global loads (including loads into LDS) have landed
+__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+// 16 bytes per lane from global memory straight into LDS (no registers): the wave
+// writes 64 consecutive 16-byte chunks starting at `lds_dst` (wave-uniform).
+__device__ __forceinline__ void global_to_lds16(const uint16_t* src, uint16_t* lds_dst) {
+    __builtin_amdgcn_global_load_lds(src, (lds_void_t*)lds_dst, 16, 0, 0);
+}
 
 // ---------------------------------------------------------------------------------
 // prefill_bf16
@@ -328,30 +380,67 @@ __global__ void __launch_bounds__(kThreads, 1) prefill_bf16(const Plan plan, con
     const uint16_t* kpool = static_cast<const uint16_t*>(a.k_pool);
     const uint16_t* vpool = static_cast<const uint16_t*>(a.v_pool);
 
-    // staging role of this thread: key kk of every tile, 16-element slice c
-    const bool stager = tid < NSTAGE;
+    // staging role of this thread (K through registers when it is rotated): key kk of
+    // every tile, 16-element slice sc
+    const bool stager = ROPE && tid < NSTAGE;
     const int kk = tid / TPK, sc = tid - (tid / TPK) * TPK;
     const int kt0 = kv_lo & ~(kBlock - 1);
     const int n_tiles = (kv_hi - kt0 + BN - 1) / BN;
+    // direct global->LDS role (V always, K too without RoPE): lane `lane` of wave
+    // `wave` fills 16-byte chunk p = (DPW*wave + i)*64 + lane of the tile, i.e. row
+    // p / CH, physical chunk p % CH, which holds logical chunk (p % CH) ^ swz(row)
+    constexpr int DPW = BN * CH / (64 * kWaves);
+    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+    auto dkey = [&](int i) { return ((DPW * wave_u + i) * 64 + lane) / CH; };
+    auto dchunk = [&](int i) {
+        const int p = (DPW * wave_u + i) * 64 + lane;
+        return (p % CH) ^ swz<D>(p / CH);
+    };
 
-    // per-key metadata one tile ahead of the data loads
-    auto load_meta = [&](int t, int& phys, int32_t& pos) {
-        const int j = kt0 + t * BN + kk;
-        phys = 0;
-        pos = 0;
-        if (stager && t < n_tiles && j >= kv_lo && j < kv_hi) {
-            phys = btab[j >> 4];
-            if (ROPE) pos = a.positions[g.pos_off + j];
+    // per-key metadata one tile ahead of the data loads: the block and position of
+    // the stager's key, and for every direct-load lane the slot (block*16 + offset)
+    // of its key -- or, for keys outside [kv_lo, kv_hi), of the tile's first visible
+    // key, so that no key outside the window is ever read (its score is masked).
+    struct Meta {
+        int phys;
+        int32_t pos;
+        int dslot[DPW];
+    };
+    auto load_meta = [&](int t, Meta& m) {
+        const int kt = kt0 + t * BN;
+        m.phys = 0;
+        m.pos = 0;
+        if (t >= n_tiles) return;
+        const int j = kt + kk;
+        if (stager && j >= kv_lo && j < kv_hi) {
+            m.phys = btab[j >> 4];
+            m.pos = a.positions[g.pos_off + j];
+        }
+        const int j_ok = max(kt, kv_lo);
+#pragma unroll
+        for (int i = 0; i < DPW; ++i) {
+            const int jd = kt + dkey(i);
+            const int jj = (jd >= kv_lo && jd < kv_hi) ? jd : j_ok;
+            m.dslot[i] = btab[jj >> 4] * kBlock + (jj & 15);
         }
     };
-    auto load_tile = [&](int t, int phys, int32_t pos, TileRegs& r) {
+    auto issue_direct = [&](int buf, const Meta& m) {
+#pragma unroll
+        for (int i = 0; i < DPW; ++i) {
+            const size_t row_off = (((size_t)(m.dslot[i] >> 4) * a.hkv + kvh) * kBlock + (m.dslot[i] & 15)) * D;
+            const int lds_off = (DPW * wave_u + i) * 64 * 8;
+            global_to_lds16(vpool + row_off + dchunk(i) * 8, &vs[buf][lds_off]);
+            if (!ROPE) global_to_lds16(kpool + row_off + dchunk(i) * 8, &ks[buf][lds_off]);
+        }
+    };
+    auto load_tile = [&](int t, const Meta& m, TileRegs& r) {
+        if (!stager) return;
         const int j = kt0 + t * BN + kk;
-        r.ok = stager && j >= kv_lo && j < kv_hi;
-        r.pos = pos;
-        r.k[0] = r.k[1] = r.v[0] = r.v[1] = u32x4_t{0, 0, 0, 0};
+        r.ok = j >= kv_lo && j < kv_hi;
+        r.pos = m.pos;
+        r.k[0] = r.k[1] = u32x4_t{0, 0, 0, 0};
         if (r.ok) {
-            const size_t row_off = (((size_t)phys * a.hkv + kvh) * kBlock + (j & 15)) * D;
-            const uint16_t* kp = kpool + row_off;
+            const uint16_t* kp = kpool + (((size_t)m.phys * a.hkv + kvh) * kBlock + (j & 15)) * D;
             if (STYLE == kNeox) {
                 r.k[0] = *reinterpret_cast<const u32x4_t*>(kp + sc * 8);
                 r.k[1] = *reinterpret_cast<const u32x4_t*>(kp + HALF + sc * 8);
@@ -359,11 +448,8 @@ __global__ void __launch_bounds__(kThreads, 1) prefill_bf16(const Plan plan, con
                 r.k[0] = *reinterpret_cast<const u32x4_t*>(kp + sc * 16);
                 r.k[1] = *reinterpret_cast<const u32x4_t*>(kp + sc * 16 + 8);
             }
-            const uint16_t* vp = vpool + row_off + sc * 16;
-            r.v[0] = *reinterpret_cast<const u32x4_t*>(vp);
-            r.v[1] = *reinterpret_cast<const u32x4_t*>(vp + 8);
-            if (ROPE && TABLE && (uint32_t)pos < (uint32_t)a.rope_len) {
-                const float4* tp = reinterpret_cast<const float4*>(a.rope_table + ((size_t)pos * HALF + sc * 8) * 2);
+            if (TABLE && (uint32_t)m.pos < (uint32_t)a.rope_len) {
+                const float4* tp = reinterpret_cast<const float4*>(a.rope_table + ((size_t)m.pos * HALF + sc * 8) * 2);
 #pragma unroll
                 for (int k = 0; k < 4; ++k) r.cs[k] = tp[k];
             }
@@ -371,147 +457,181 @@ __global__ void __launch_bounds__(kThreads, 1) prefill_bf16(const Plan plan, con
     };
     auto store_tile = [&](int buf, TileRegs& r) {
         if (!stager) return;
-        if (ROPE && r.ok) {
-            float c[8], s[8];
-            if (TABLE && (uint32_t)r.pos < (uint32_t)a.rope_len) {
+        // e[k] = (cos, -sin | sin, cos) of pair sc*8 + k as bf16: from the table, or
+        // computed for keys whose position lies outside it (a wave-uniform branch, so
+        // the common all-in-table case runs no fallback code)
+        uint2 e[8];
 #pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    c[2 * k] = r.cs[k].x; s[2 * k] = r.cs[k].y; c[2 * k + 1] = r.cs[k].z; s[2 * k + 1] = r.cs[k].w;
+        for (int k = 0; k < 4; ++k) {
+            e[2 * k] = make_uint2(__float_as_uint(r.cs[k].x), __float_as_uint(r.cs[k].y));
+            e[2 * k + 1] = make_uint2(__float_as_uint(r.cs[k].z), __float_as_uint(r.cs[k].w));
+        }
+        const bool need_cs = r.ok && !(TABLE && (uint32_t)r.pos < (uint32_t)a.rope_len);
+        if (!TABLE || __builtin_amdgcn_ballot_w64(need_cs) != 0) {
+            if (need_cs) {
+#pragma unroll
+                for (int k = 0; k < 8; ++k) {
+                    float c, sn;
+                    rope_cs(r.pos, fstep[sc * 8 + k], c, sn);
+                    e[k] = bf16_entry(c, sn);
                 }
-            } else {
-#pragma unroll
-                for (int k = 0; k < 8; ++k) rope_cs(r.pos, fstep[sc * 8 + k], c[k], s[k]);
-            }
-            if (STYLE == kNeox) {
-#pragma unroll
-                for (int m = 0; m < 4; ++m) {
-                    const float x0 = bf_lo(r.k[0][m]), x1 = bf_hi(r.k[0][m]);
-                    const float y0 = bf_lo(r.k[1][m]), y1 = bf_hi(r.k[1][m]);
-                    const float c0 = c[2 * m], c1 = c[2 * m + 1], s0 = s[2 * m], s1 = s[2 * m + 1];
-                    r.k[0][m] = pack_bf16(x0 * c0 - y0 * s0, x1 * c1 - y1 * s1);
-                    r.k[1][m] = pack_bf16(y0 * c0 + x0 * s0, y1 * c1 + x1 * s1);
-                }
-            } else {
-#pragma unroll
-                for (int h2 = 0; h2 < 2; ++h2)
-#pragma unroll
-                    for (int m = 0; m < 4; ++m) {
-                        const float x = bf_lo(r.k[h2][m]), y = bf_hi(r.k[h2][m]);
-                        const float cc = c[4 * h2 + m], ss = s[4 * h2 + m];
-                        r.k[h2][m] = pack_bf16(x * cc - y * ss, y * cc + x * ss);
-                    }
             }
         }
-        const int sw = kk & (CH - 1);
+        if (STYLE == kNeox) {
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+                const uint32_t A = r.k[0][m], B = r.k[1][m];
+                const uint32_t p0 = (A & 0xffffu) | (B << 16);        // (x_2m, y_2m)
+                const uint32_t p1 = (A >> 16) | (B & 0xffff0000u);    // (x_2m+1, y_2m+1)
+                const float x0 = dot2_bf16(p0, e[2 * m].x), y0 = dot2_bf16(p0, e[2 * m].y);
+                const float x1 = dot2_bf16(p1, e[2 * m + 1].x), y1 = dot2_bf16(p1, e[2 * m + 1].y);
+                r.k[0][m] = pack_bf16(x0, x1);
+                r.k[1][m] = pack_bf16(y0, y1);
+            }
+        } else {
+#pragma unroll
+            for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+                for (int m = 0; m < 4; ++m) {
+                    const uint32_t xy = r.k[h2][m];
+                    const uint2 ee = e[4 * h2 + m];
+                    r.k[h2][m] = pack_bf16(dot2_bf16(xy, ee.x), dot2_bf16(xy, ee.y));
+                }
+        }
+        // keys outside the window (partial tiles only) are stored as zeros
+        if (__builtin_amdgcn_ballot_w64(!r.ok) != 0) {
+            if (!r.ok) r.k[0] = r.k[1] = u32x4_t{0, 0, 0, 0};
+        }
+        const int sw = swz<D>(kk);
         uint16_t* krow = &ks[buf][kk * D];
-        uint16_t* vrow = &vs[buf][kk * D];
         const int ca = STYLE == kNeox ? sc : 2 * sc;
         const int cb = STYLE == kNeox ? sc + CH / 2 : 2 * sc + 1;
         *reinterpret_cast<u32x4_t*>(krow + ((ca ^ sw) << 3)) = r.k[0];
         *reinterpret_cast<u32x4_t*>(krow + ((cb ^ sw) << 3)) = r.k[1];
-        *reinterpret_cast<u32x4_t*>(vrow + (((2 * sc) ^ sw) << 3)) = r.v[0];
-        *reinterpret_cast<u32x4_t*>(vrow + (((2 * sc + 1) ^ sw) << 3)) = r.v[1];
     };
 
     TileRegs regs;
-    int phys_n, phys_nn;
-    int32_t pos_n, pos_nn;
-    load_meta(0, phys_n, pos_n);
-    load_tile(0, phys_n, pos_n, regs);
-    load_meta(1, phys_nn, pos_nn);
+    Meta meta_n, meta_nn;
+    load_meta(0, meta_n);
+    issue_direct(0, meta_n);
+    load_tile(0, meta_n, regs);
+    load_meta(1, meta_nn);
     store_tile(0, regs);
+    wait_vmem();
     __syncthreads();
 
-    for (int t = 0; t < n_tiles; ++t) {
-        const int buf = t & 1;
+    // per-lane LDS element offsets, constant over tiles: the K operand row of each
+    // contraction step, and the V^T operand rows (keys 4*(l/32)+{0..3} and the same
+    // +8 of a 16-key step) of each 32-dim block.  Buffer, 32-key half and 16-key step
+    // add compile-time constants (the swizzle only depends on a key's low 4 bits).
+    int k_off[KD];
+#pragma unroll
+    for (int kd = 0; kd < KD; ++kd) k_off[kd] = l32 * D + (((kd * 2 + hi) ^ swz<D>(l32)) << 3);
+    int v_off[DB];
+    {
+        const int q16 = (lane >> 4) & 1, kq = (lane & 15) >> 2, dq = 4 * (lane & 3);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+            const int key = 4 * hi + kq;
+            const int d = db * 32 + q16 * 16 + dq;
+            v_off[db] = key * D + (((d >> 3) ^ swz<D>(key)) << 3) + (d & 7);
+        }
+    }
+    // the same lane's row 8 keys further: swz(key + 8) = swz(key) ^ kSwz8
+    constexpr int kSwz8 = D == 128 ? 2 : 4;
+    static_assert(D == 64 || D == 128, "head_dim");
+    const int hi_key = min(kv_hi - 1, row_tok);   // last key this lane's row may see
+
+    auto step = [&](auto bufc, int t) {
+        constexpr int buf = decltype(bufc)::value;
         const int kt = kt0 + t * BN;
         const bool more = t + 1 < n_tiles;
-        if (more) {
-            load_tile(t + 1, phys_nn, pos_nn, regs);
-            load_meta(t + 2, phys_nn, pos_nn);
-        }
+        // direct loads of the next tile (no registers) go out first; the rotated-K
+        // register loads wait until the score tile is dead (after the softmax)
+        if (more) issue_direct(buf ^ 1, meta_nn);
         if (wave_live) {
-            // ---- S^T = K Q^T
-            f32x16_t s[2] = {f32x16_t{}, f32x16_t{}};
-#pragma unroll
-            for (int kd = 0; kd < KD; ++kd)
-#pragma unroll
-                for (int mb = 0; mb < 2; ++mb) {
-                    const int kr = mb * 32 + l32;
-                    const bf16x8_t af = *reinterpret_cast<const bf16x8_t*>(
-                        &ks[buf][kr * D + (((kd * 2 + hi) ^ (kr & (CH - 1))) << 3)]);
-                    s[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, qb[kd], s[mb], 0, 0, 0);
-                }
-            // ---- window mask, only on tiles that cross a boundary of the visible set
-            if (kt < kv_lo || kt + BN > kv_hi || kt + BN - 1 > wave_tmin) {
-#pragma unroll
-                for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-                    for (int j = 0; j < 16; ++j) {
-                        const int key = kt + mb * 32 + 8 * (j >> 2) + 4 * hi + (j & 3);
-                        if (key < kv_lo || key >= kv_hi || key > row_tok) s[mb][j] = -INFINITY;
-                    }
-            }
-            // ---- online softmax in the log2 domain.  The reference maximum only moves
-            // when some row's maximum grows by more than 8 (probabilities stay below 2^8),
-            // so most tiles skip rescaling the accumulators.
-            float mx = kNegBig;
-#pragma unroll
-            for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-                for (int j = 0; j < 16; ++j) mx = fmaxf(mx, s[mb][j]);
-            mx = max_xor32(mx);
-            if (__builtin_amdgcn_ballot_w64(mx > m_run + 8.f) != 0) {
-                const float m_new = fmaxf(m_run, mx);
-                const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-                l_run *= alpha;
-#pragma unroll
-                for (int db = 0; db < DB; ++db) acc[db] *= alpha;
-                m_run = m_new;
-            }
-            bf16x8_t pb[2][2];
+            const uint16_t* kb = &ks[buf][0];
+            lds_u16_t* vb = as_lds(&vs[buf][0]);
+            const bool masked = kt < kv_lo || kt + BN > kv_hi || kt + BN - 1 > wave_tmin;
+            // the tile is consumed as two 32-key halves: S^T half -> mask -> softmax ->
+            // O^T += V^T P^T half; the second half's QK^T does not depend on the first
+            // half's softmax, which leaves MFMA work to overlap with VALU work
 #pragma unroll
             for (int mb = 0; mb < 2; ++mb) {
+                // ---- S^T (32 keys x 32 queries) = K Q^T
+                f32x16_t s = f32x16_t{};
 #pragma unroll
-                for (int j = 0; j < 16; ++j) {
-                    const float p = __builtin_amdgcn_exp2f(s[mb][j] - m_run);
-                    s[mb][j] = p;
-                    l_run += p;
+                for (int kd = 0; kd < KD; ++kd) {
+                    const bf16x8_t af = *reinterpret_cast<const bf16x8_t*>(kb + k_off[kd] + mb * 32 * D);
+                    s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, qb[kd], s, 0, 0, 0);
                 }
+                // ---- window mask on tiles that cross a boundary of the visible set: a
+                // bit mask of the visible keys relative to this lane's first key
+                if (masked) {
+                    const int base = kt + mb * 32 + 4 * hi;
+                    const int lo = max(kv_lo - base, 0), top = min(hi_key - base, 31);
+                    const uint32_t upto = (2u << (uint32_t)max(top, 0)) - 1u;
+                    const uint32_t vis = (top < lo) ? 0u : (upto & ~((1u << (uint32_t)min(lo, 31)) - 1u));
+#pragma unroll
+                    for (int j = 0; j < 16; ++j) {
+                        const int c = 8 * (j >> 2) + (j & 3);
+                        s[j] = (vis & (1u << c)) ? s[j] : -INFINITY;
+                    }
+                }
+                // ---- online softmax in the log2 domain.  The reference maximum only
+                // moves when some row's maximum grows by more than 8 (probabilities stay
+                // below 2^8), so most halves skip rescaling the accumulators.
+                float mx = kNegBig;
+#pragma unroll
+                for (int j = 0; j < 16; ++j) mx = fmaxf(mx, s[j]);
+                mx = max_xor32(mx);
+                if (__builtin_amdgcn_ballot_w64(mx > m_run + 8.f) != 0) {
+                    const float m_new = fmaxf(m_run, mx);
+                    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+                    l_run *= alpha;
+#pragma unroll
+                    for (int db = 0; db < DB; ++db) acc[db] *= alpha;
+                    m_run = m_new;
+                }
+                // probabilities: fp32 for the row sum, bf16 for P V
+                bf16x8_t pb[2];
 #pragma unroll
                 for (int k2 = 0; k2 < 2; ++k2) {
                     u32x4_t w;
 #pragma unroll
-                    for (int m = 0; m < 4; ++m) w[m] = pack_bf16(s[mb][8 * k2 + 2 * m], s[mb][8 * k2 + 2 * m + 1]);
-                    pb[mb][k2] = __builtin_bit_cast(bf16x8_t, w);
+                    for (int m = 0; m < 4; ++m) {
+                        const float p0 = __builtin_amdgcn_exp2f(s[8 * k2 + 2 * m] - m_run);
+                        const float p1 = __builtin_amdgcn_exp2f(s[8 * k2 + 2 * m + 1] - m_run);
+                        l_run += p0 + p1;
+                        w[m] = pack_bf16(p0, p1);
+                    }
+                    pb[k2] = __builtin_bit_cast(bf16x8_t, w);
                 }
-            }
-            // ---- O^T += V^T P^T; the A operand rows are dims, its 8 keys per lane are
-            // keys 16*k2 + 4*(l/32) + {0..3} and the same + 8 of each 32-key half
-            const int q16 = (lane >> 4) & 1;
-            const int kq = (lane & 15) >> 2;
-            const int dq = 4 * (lane & 3);
+                if (mb == 1 && more) load_tile(t + 1, meta_nn, regs);
+                // ---- O^T += V^T P^T
 #pragma unroll
-            for (int db = 0; db < DB; ++db) {
-                const int d = db * 32 + q16 * 16 + dq;
-#pragma unroll
-                for (int mb = 0; mb < 2; ++mb)
+                for (int db = 0; db < DB; ++db)
 #pragma unroll
                     for (int k2 = 0; k2 < 2; ++k2) {
-                        const int key0 = mb * 32 + 16 * k2 + 4 * hi + kq;
-                        const int key1 = key0 + 8;
-                        const s16x4_t lo = lds_read_tr(
-                            &vs[buf][key0 * D + (((d >> 3) ^ (key0 & (CH - 1))) << 3) + (d & 7)]);
-                        const s16x4_t up = lds_read_tr(
-                            &vs[buf][key1 * D + (((d >> 3) ^ (key1 & (CH - 1))) << 3) + (d & 7)]);
-                        const s16x4_t both[2] = {lo, up};
+                        const int row0 = (mb * 32 + 16 * k2) * D;
+                        const s16x4_t both[2] = {lds_read_tr(vb + v_off[db] + row0),
+                                                 lds_read_tr(vb + (v_off[db] ^ (kSwz8 << 3)) + 8 * D + row0)};
                         const bf16x8_t af = __builtin_bit_cast(bf16x8_t, both);
-                        acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, pb[mb][k2], acc[db], 0, 0, 0);
+                        acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, pb[k2], acc[db], 0, 0, 0);
                     }
             }
         }
-        if (more) store_tile(buf ^ 1, regs);
+        if (more) {
+            if (!wave_live) load_tile(t + 1, meta_nn, regs);
+            load_meta(t + 2, meta_nn);
+            store_tile(buf ^ 1, regs);
+        }
+        wait_vmem();
         __syncthreads();
+    };
+    for (int t = 0; t < n_tiles; t += 2) {
+        step(std::integral_constant<int, 0>{}, t);
+        if (t + 1 < n_tiles) step(std::integral_constant<int, 1>{}, t + 1);
     }
 
     // ---- epilogue: normalise and store, or store the split's partial state
@@ -731,11 +851,11 @@ int launch_kv_write(int dtype, int hkv, int d, void* k_pool, void* v_pool, const
     return hipGetLastError();
 }
 
-int launch_rope_table(int d, double theta, int n_pos, float* table, void* stream) {
+int launch_rope_table(int dtype, int d, double theta, int n_pos, float* table, void* stream) {
     const int64_t n = (int64_t)n_pos * (d / 2);
     if (n == 0) return hipSuccess;
     hipLaunchKernelGGL(rope_table_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, (hipStream_t)stream,
-                       reinterpret_cast<float2*>(table), n_pos, d / 2, d, theta);
+                       reinterpret_cast<uint2*>(table), n_pos, d / 2, d, theta, dtype != 1);
     return hipGetLastError();
 }
 
@@ -744,7 +864,7 @@ int launch_rope_rotate(int dtype, int style, int d, double theta, const float* t
     const int64_t n_pairs = (int64_t)n * heads * (d / 2);
     if (n_pairs == 0) return hipSuccess;
     const dim3 grid((unsigned)((n_pairs + 255) / 256));
-    const float2* t = reinterpret_cast<const float2*>(table);
+    const uint2* t = reinterpret_cast<const uint2*>(table);
     hipStream_t st = (hipStream_t)stream;
     if (dtype == 1) {
         if (style == kNeox)
