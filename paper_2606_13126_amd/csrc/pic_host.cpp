@@ -147,27 +147,28 @@ pic_status make_plan(const pic_config* c, const pic_batch_host* b, bool decode, 
             g.split_keys = 0;
         }
     } else {
-        // split keys only when the unsplit items cannot fill the chip
-        int64_t base = 0, work = 0;
+        // Key splits, counted in 64-key tiles.  Split when the unsplit items cannot
+        // fill the chip (chunks of the average work per CU), or when some item is
+        // much longer than the average work per CU, which would leave its CU running
+        // alone at the end (chunks of a third of that average).
+        int64_t base = 0, tiles_total = 0, max_item = 0;
         for (auto& g : hp.groups) {
             g.n_rt = (int32_t)(((int64_t)g.n_tok * G + pic::kTileRows - 1) / pic::kTileRows);
-            const int64_t keys = (int64_t)g.tok0 + g.n_tok - g.win;
+            const int64_t tiles = ((int64_t)g.tok0 + g.n_tok - g.win + pic::kTileKeys - 1) / pic::kTileKeys;
             base += (int64_t)g.n_rt * c->num_kv_heads;
-            work += (int64_t)g.n_rt * c->num_kv_heads * keys;
+            tiles_total += (int64_t)g.n_rt * c->num_kv_heads * tiles;
+            max_item = std::max(max_item, tiles);
         }
-        int64_t chunk = INT32_MAX;
-        if (base < pic::kTargetCUs && work > 0)
-            chunk = std::max<int64_t>(4 * pic::kTileKeys, round_up((work + pic::kTargetCUs - 1) / pic::kTargetCUs,
-                                                                   pic::kTileKeys));
+        const double avg = (double)tiles_total / pic::kTargetCUs;
+        int64_t cap = INT32_MAX;
+        if (base < pic::kTargetCUs)
+            cap = std::max<int64_t>(4, (int64_t)std::ceil(avg));
+        else if ((double)max_item > 1.25 * avg)
+            cap = std::max<int64_t>(32, (int64_t)std::ceil(avg / 3.0));
         for (auto& g : hp.groups) {
-            const int64_t keys = (int64_t)g.tok0 + g.n_tok - g.win;
-            if (keys <= chunk) {
-                g.n_split = 1;
-                g.split_keys = round_up(keys, pic::kTileKeys);
-            } else {
-                g.n_split = (int32_t)((keys + chunk - 1) / chunk);
-                g.split_keys = (int32_t)chunk;
-            }
+            const int64_t tiles = ((int64_t)g.tok0 + g.n_tok - g.win + pic::kTileKeys - 1) / pic::kTileKeys;
+            g.n_split = (int32_t)((tiles + cap - 1) / cap);
+            g.split_keys = (int32_t)(((tiles + g.n_split - 1) / g.n_split) * pic::kTileKeys);
         }
         // heaviest items first
         std::stable_sort(hp.groups.begin(), hp.groups.end(), [](const pic::Group& x, const pic::Group& y) {
@@ -203,7 +204,7 @@ void make_launches(const pic_config* c, HostPlan& hp, std::vector<pic::Plan>& la
                 g.part_base = (int32_t)part;
                 part += (int64_t)g.n_rt * c->num_kv_heads * g.n_split;
                 g.merge_base = (int32_t)merge;
-                merge += (int64_t)g.n_rt * c->num_kv_heads * (pic::kTileRows / 32);
+                merge += (int64_t)g.n_rt * c->num_kv_heads * (pic::kTileRows / pic::kMergeRows);
             }
             p.g[p.n_groups++] = g;
             ++i;

@@ -12,6 +12,7 @@ constexpr int kTileRows = 256;    // query rows (token x head-in-group) per pref
 constexpr int kTileKeys = 64;     // keys per K/V tile of the prefill kernel
 constexpr int kMaxGroups = 64;    // groups passed by value in one launch
 constexpr int kTargetCUs = 256;   // MI355X compute units the split policy fills
+constexpr int kMergeRows = 8;     // rows per block of the split merge
 
 // One query span of one request (prefill) or one request's last token (decode).
 // Its work items are (row tile, KV head, key split) triples, enumerated from

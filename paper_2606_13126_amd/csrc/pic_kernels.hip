@@ -667,16 +667,18 @@ __global__ void __launch_bounds__(kThreads, 1) prefill_bf16(const Plan plan, con
 
 // ---------------------------------------------------------------------------------
 // merge: O = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s over the non-empty splits
-// of one (row tile, KV head); one block per 32 rows, 8 threads per row.
+// of one (row tile, KV head), as a streaming log-sum-exp merge.  One block per
+// kMergeRows rows, one float4 of a row per thread; the loads of 8 splits are issued
+// together before they are combined.
 // ---------------------------------------------------------------------------------
-constexpr int kMergeRows = 32;
-
 template <int D>
-__global__ void __launch_bounds__(256) merge_kernel(const Plan plan, const Args a) {
+__global__ void __launch_bounds__(kMergeRows * D / 4) merge_kernel(const Plan plan, const Args a) {
+    constexpr int TPR = D / 4;                      // threads per row
+    constexpr int CHUNKS = kTileRows / kMergeRows;  // blocks per (row tile, KV head)
+    constexpr int U = 8;                            // splits loaded per batch
     const int gi = find_merge_group(plan, blockIdx.x);
     if (gi < 0) return;
     const Group g = plan.g[gi];
-    constexpr int CHUNKS = kTileRows / kMergeRows;
     int li = blockIdx.x - g.merge_base;
     if (li >= a.hkv * g.n_rt * CHUNKS) return;
     const int chunk = li % CHUNKS;
@@ -689,40 +691,45 @@ __global__ void __launch_bounds__(256) merge_kernel(const Plan plan, const Args 
     int n_live = 0;
     for (int s = 0; s < g.n_split; ++s)
         if (g.win + s * g.split_keys < t_last + 1) n_live = s + 1;
-    const int r = chunk * kMergeRows + (int)threadIdx.x / 8;
+    const int r = chunk * kMergeRows + (int)threadIdx.x / TPR;
+    const int q4 = (int)threadIdx.x % TPR;
     if (row_lo + r >= row_hi) return;
-    constexpr int PER = D / 8;   // floats per thread
-    const int d0 = ((int)threadIdx.x & 7) * PER;
-    float mmax = kNegBig;
-    for (int s = 0; s < n_live; ++s) {
-        const size_t slot = (size_t)g.part_base + ((size_t)kvh * g.n_split + s) * g.n_rt + rt;
-        const float2 ml = *reinterpret_cast<const float2*>(a.part_ml + (slot * kTileRows + r) * 2);
-        if (ml.y > 0.f) mmax = fmaxf(mmax, ml.x);
-    }
-    float num[PER];
+    const size_t slot0 = (size_t)g.part_base + (size_t)kvh * g.n_split * g.n_rt + rt;
+    float M = kNegBig, den = 0.f;
+    float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int s0 = 0; s0 < n_live; s0 += U) {
+        float2 ml[U];
+        float4 v[U];
 #pragma unroll
-    for (int e = 0; e < PER; ++e) num[e] = 0.f;
-    float den = 0.f;
-    for (int s = 0; s < n_live; ++s) {
-        const size_t slot = (size_t)g.part_base + ((size_t)kvh * g.n_split + s) * g.n_rt + rt;
-        const float2 ml = *reinterpret_cast<const float2*>(a.part_ml + (slot * kTileRows + r) * 2);
-        if (!(ml.y > 0.f)) continue;
-        const float w = __builtin_amdgcn_exp2f(ml.x - mmax);
-        const float4* v = reinterpret_cast<const float4*>(a.part_o + (slot * kTileRows + r) * D + d0);
-#pragma unroll
-        for (int e = 0; e < PER / 4; ++e) {
-            const float4 x = v[e];
-            num[4 * e] += w * x.x; num[4 * e + 1] += w * x.y; num[4 * e + 2] += w * x.z; num[4 * e + 3] += w * x.w;
+        for (int u = 0; u < U; ++u) {
+            ml[u] = make_float2(kNegBig, 0.f);
+            v[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (s0 + u < n_live) {
+                const size_t slot = slot0 + (size_t)(s0 + u) * g.n_rt;
+                ml[u] = *reinterpret_cast<const float2*>(a.part_ml + (slot * kTileRows + r) * 2);
+                v[u] = *reinterpret_cast<const float4*>(a.part_o + (slot * kTileRows + r) * D + q4 * 4);
+            }
         }
-        den += w * ml.y;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (!(ml[u].y > 0.f)) continue;   // split saw no key of this row
+            const float m_new = fmaxf(M, ml[u].x);
+            const float c_old = __builtin_amdgcn_exp2f(M - m_new), c_new = __builtin_amdgcn_exp2f(ml[u].x - m_new);
+            num.x = num.x * c_old + c_new * v[u].x;
+            num.y = num.y * c_old + c_new * v[u].y;
+            num.z = num.z * c_old + c_new * v[u].z;
+            num.w = num.w * c_old + c_new * v[u].w;
+            den = den * c_old + c_new * ml[u].y;
+            M = m_new;
+        }
     }
     const float inv = 1.f / den;
     const int row = row_lo + r;
     const int toff = row / G, hl = row - toff * G;
     uint32_t* op = reinterpret_cast<uint32_t*>(static_cast<uint16_t*>(a.o) +
-                                               ((size_t)(g.q_row0 + toff) * a.hq + (size_t)kvh * G + hl) * D + d0);
-#pragma unroll
-    for (int e = 0; e < PER / 2; ++e) op[e] = pack_bf16(num[2 * e] * inv, num[2 * e + 1] * inv);
+                                               ((size_t)(g.q_row0 + toff) * a.hq + (size_t)kvh * G + hl) * D + q4 * 4);
+    op[0] = pack_bf16(num.x * inv, num.y * inv);
+    op[1] = pack_bf16(num.z * inv, num.w * inv);
 }
 
 // ---------------------------------------------------------------------------------
@@ -821,7 +828,7 @@ hipError_t launch_attn_t(int dtype, const Plan& plan, const Args& a, hipStream_t
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (plan.n_merge > 0) {
-        hipLaunchKernelGGL((merge_kernel<D>), dim3(plan.n_merge), dim3(256), 0, st, plan, a);
+        hipLaunchKernelGGL((merge_kernel<D>), dim3(plan.n_merge), dim3(kMergeRows * D / 4), 0, st, plan, a);
         e = hipGetLastError();
     }
     return e;
