@@ -14,10 +14,13 @@
 #include <string>
 #include <vector>
 
-#include "../../include/pic_attn.h"
+#include "pic_attn.h"
 #include "pic_internal.h"
 
 namespace {
+
+// both structures travel as kernel arguments
+static_assert(sizeof(pic::Plan) + sizeof(pic::Args) <= 4096, "kernel arguments must stay within 4 KB");
 
 thread_local std::string g_error;
 
@@ -193,6 +196,7 @@ void make_launches(const pic_config* c, HostPlan& hp, std::vector<pic::Plan>& la
     while (i < hp.groups.size()) {
         pic::Plan p;
         std::memset(&p, 0, sizeof(p));
+        p.part0 = (int32_t)part;
         int64_t item = 0, merge = 0;
         while (i < hp.groups.size() && p.n_groups < pic::kMaxGroups) {
             pic::Group g = hp.groups[i];
@@ -201,9 +205,7 @@ void make_launches(const pic_config* c, HostPlan& hp, std::vector<pic::Plan>& la
             g.item_base = (int32_t)item;
             item += round_up(n, 8);
             if (c->dtype != PIC_F32 && g.n_split > 1) {
-                g.part_base = (int32_t)part;
                 part += (int64_t)g.n_rt * c->num_kv_heads * g.n_split;
-                g.merge_base = (int32_t)merge;
                 merge += (int64_t)g.n_rt * c->num_kv_heads * (pic::kTileRows / pic::kMergeRows);
             }
             p.g[p.n_groups++] = g;
@@ -218,6 +220,18 @@ void make_launches(const pic_config* c, HostPlan& hp, std::vector<pic::Plan>& la
 
 size_t workspace_bytes(const pic_config* c, int64_t n_parts) {
     return (size_t)n_parts * pic::kTileRows * ((size_t)c->head_dim + 2) * sizeof(float);
+}
+
+// Phase step of RoPE pair i: omega_i / 2pi revolutions per position as a 64-bit
+// binary fraction, in long double so that the rounding of omega_i stays far below
+// the 2^-64 step.
+void phase_steps(int head_dim, double theta, uint64_t* out) {
+    const long double two_pi = 6.283185307179586476925286766559L;
+    for (int i = 0; i < head_dim / 2; ++i) {
+        long double rev = powl((long double)theta, -2.0L * i / head_dim) / two_pi;
+        rev -= floorl(rev);
+        out[i] = (uint64_t)(rev * 18446744073709551616.0L);
+    }
 }
 
 pic_status hip_status(int e, const char* what) {
@@ -254,6 +268,7 @@ pic_status run_attention(const pic_config* c, const pic_batch_host* b, const pic
         return fail(PIC_EWORKSPACE, "workspace needs " + std::to_string(need) + " bytes");
 
     pic::Args a{};
+    phase_steps(c->head_dim, c->rope_theta, a.fstep);
     a.q = q;
     a.o = o;
     a.k_pool = k_pool;
@@ -379,7 +394,8 @@ pic_status pic_plan_debug(const pic_config* cfg, const pic_batch_host* batch, in
         }
         ++n;
     };
-    for (const auto& p : launches)
+    for (const auto& p : launches) {
+        int64_t part_base = p.part0;
         for (int gi = 0; gi < p.n_groups; ++gi) {
             const pic::Group& g = p.g[gi];
             if (cfg->dtype == PIC_F32) {
@@ -400,10 +416,12 @@ pic_status pic_plan_debug(const pic_config* cfg, const pic_batch_host* batch, in
                         const int32_t kh = std::min(kl + g.split_keys, t_last + 1);
                         if (kl >= kh) continue;
                         const int32_t slot =
-                            g.n_split > 1 ? g.part_base + (kvh * g.n_split + s) * g.n_rt + rt : -1;
+                            g.n_split > 1 ? (int32_t)part_base + (kvh * g.n_split + s) * g.n_rt + rt : -1;
                         emit(g.req, kvh, rl, rh, kl, kh, g.tok0, slot);
                     }
+            if (g.n_split > 1) part_base += (int64_t)g.n_rt * cfg->num_kv_heads * g.n_split;
         }
+    }
     *n_items = (int32_t)std::min<int64_t>(n, INT32_MAX);
     return PIC_OK;
 }

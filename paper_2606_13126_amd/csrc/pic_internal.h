@@ -8,15 +8,23 @@
 namespace pic {
 
 constexpr int kBlock = 16;        // tokens per KV block
-constexpr int kTileRows = 256;    // query rows (token x head-in-group) per prefill workgroup
-constexpr int kTileKeys = 64;     // keys per K/V tile of the prefill kernel
-constexpr int kMaxGroups = 64;    // groups passed by value in one launch
+#ifndef PIC_TILE_ROWS
+#define PIC_TILE_ROWS 256
+#endif
+#ifndef PIC_TILE_KEYS
+#define PIC_TILE_KEYS 64
+#endif
+constexpr int kTileRows = PIC_TILE_ROWS;  // query rows (token x head-in-group) per prefill workgroup
+constexpr int kTileKeys = PIC_TILE_KEYS;  // keys per K/V tile of the prefill kernel
+constexpr int kMaxGroups = 72;    // groups passed by value in one launch (kernel arguments < 4 KB)
 constexpr int kTargetCUs = 256;   // MI355X compute units the split policy fills
 constexpr int kMergeRows = 8;     // rows per block of the split merge
 
 // One query span of one request (prefill) or one request's last token (decode).
 // Its work items are (row tile, KV head, key split) triples, enumerated from
-// item_base; partial results of split items live at part_base onwards.
+// item_base.  Partial results of split groups take consecutive slots in group
+// order from Plan::part0, and their merge blocks consecutive block indices; the
+// kernels recover both bases by summing over the preceding groups.
 struct Group {
     int32_t req;         // request index (row of the block table)
     int32_t tok0;        // sequence index of the span's first query token
@@ -28,19 +36,20 @@ struct Group {
     int32_t n_split;     // key splits per (row tile, KV head)
     int32_t split_keys;  // keys per split (a multiple of kTileKeys)
     int32_t item_base;   // first item (block index) of the group; a multiple of 8
-    int32_t part_base;   // first partial slot (n_split > 1)
-    int32_t merge_base;  // first merge block (n_split > 1)
 };
 
 struct Plan {
     int32_t n_groups;
     int32_t n_items;     // blocks of the attention launch
     int32_t n_merge;     // blocks of the merge launch
-    int32_t pad_;
+    int32_t part0;       // first partial slot of this launch's split groups
     Group g[kMaxGroups];
 };
 
 struct Args {
+    // RoPE phase step of pair i as a 64-bit fraction of a revolution per position:
+    // round(frac(omega_i / 2pi) * 2^64), omega_i = theta^(-2i/D)
+    uint64_t fstep[64];
     const void* q;
     void* o;
     const void* k_pool;

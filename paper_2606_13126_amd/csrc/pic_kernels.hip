@@ -171,21 +171,44 @@ __global__ void __launch_bounds__(256) rope_rotate_kernel(T* __restrict__ x, int
     row[ib] = (T)(b * c + a * s);
 }
 
-// Locate the group of a block: groups are sorted by item_base.
-__device__ __forceinline__ int find_group(const Plan& plan, int bid) {
-    int gi = 0;
-    while (gi + 1 < plan.n_groups && plan.g[gi + 1].item_base <= bid) ++gi;
+// Partial slots and merge blocks of a split group.
+__device__ __forceinline__ int group_parts(const Group& x, int hkv) {
+    return x.n_split > 1 ? x.n_rt * hkv * x.n_split : 0;
+}
+__device__ __forceinline__ int group_merges(const Group& x, int hkv) {
+    return x.n_split > 1 ? x.n_rt * hkv * (kTileRows / kMergeRows) : 0;
+}
+
+// Group of an attention block (groups are sorted by item_base) and its first
+// partial slot.
+__device__ __forceinline__ int find_group(const Plan& plan, int bid, int hkv, int& part_base) {
+    int gi = 0, part = plan.part0;
+    while (gi + 1 < plan.n_groups && plan.g[gi + 1].item_base <= bid) {
+        part += group_parts(plan.g[gi], hkv);
+        ++gi;
+    }
+    part_base = part;
     return gi;
 }
 
-__device__ __forceinline__ int find_merge_group(const Plan& plan, int bid) {
-    int gi = -1;
-    for (int i = 0; i < plan.n_groups; ++i)
-        if (plan.g[i].n_split > 1 && plan.g[i].merge_base <= bid) gi = i;
-    return gi;
+// Group of a merge block, its first partial slot and its first merge block.
+__device__ __forceinline__ int find_merge_group(const Plan& plan, int bid, int hkv, int& part_base,
+                                                int& merge_base) {
+    int part = plan.part0, merge = 0;
+    for (int i = 0; i < plan.n_groups; ++i) {
+        const int nb = group_merges(plan.g[i], hkv);
+        if (bid < merge + nb) {
+            part_base = part;
+            merge_base = merge;
+            return i;
+        }
+        merge += nb;
+        part += group_parts(plan.g[i], hkv);
+    }
+    return -1;
 }
 
-constexpr int kWaves = kTileRows / 32;   // 8 waves, 2 per SIMD; wave w owns rows [32w, 32w+32)
+constexpr int kWaves = kTileRows / 32;   // wave w owns rows [32w, 32w+32); 2 waves per SIMD
 constexpr int kThreads = kWaves * 64;
 
 // max over lanes l and l^32 (one VALU permute, no LDS round trip)
@@ -261,7 +284,7 @@ __device__ __forceinline__ void global_to_lds16(const uint16_t* src, uint16_t* l
 //   straight from the untransposed V tile through ds_read_b64_tr_b16.
 // ---------------------------------------------------------------------------------
 template <int D, int STYLE, bool ROPE, bool TABLE>
-__global__ void __launch_bounds__(kThreads, 1) prefill_bf16(const Plan plan, const Args a) {
+__global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const Plan plan, const Args a) {
     constexpr int KD = D / 16;    // 16-wide contraction steps of QK^T
     constexpr int DB = D / 32;    // 32-row blocks of O^T
     constexpr int CH = D / 8;     // 16-byte chunks per row
@@ -269,6 +292,9 @@ __global__ void __launch_bounds__(kThreads, 1) prefill_bf16(const Plan plan, con
     constexpr int BN = kTileKeys;
     constexpr int TPK = D / 16;   // staging threads per key
     constexpr int NSTAGE = BN * TPK;
+    constexpr int SU = NSTAGE > kThreads ? NSTAGE / kThreads : 1;   // staged keys per thread
+    constexpr int NH = BN / 32;                                      // 32-key halves per tile
+    static_assert(BN % 32 == 0 && (NSTAGE <= kThreads || NSTAGE % kThreads == 0), "tile shape");
 
     __shared__ __attribute__((aligned(16))) uint16_t ks[2][BN * D];
     __shared__ __attribute__((aligned(16))) uint16_t vs[2][BN * D];
@@ -278,7 +304,8 @@ __global__ void __launch_bounds__(kThreads, 1) prefill_bf16(const Plan plan, con
     const int l32 = lane & 31, hi = lane >> 5;
 
     const int bid = blockIdx.x;
-    const Group g = plan.g[find_group(plan, bid)];
+    int part_base;
+    const Group g = plan.g[find_group(plan, bid, a.hkv, part_base)];
     const int G = a.group;
     const int n_clusters = a.hkv * g.n_split;
     const int li = bid - g.item_base;
@@ -303,9 +330,13 @@ __global__ void __launch_bounds__(kThreads, 1) prefill_bf16(const Plan plan, con
     const int kv_hi = min(kv_lo + g.split_keys, t_last + 1);
     if (kv_lo >= kv_hi) return;
 
-    if (ROPE) {
-        for (int i = tid; i < HALF; i += kThreads) fstep[i] = rope_phase_step(a.theta, i, D);
+    // phase steps of the in-kernel cos/sin: staged in LDS when every position needs
+    // them (no table); with a table only positions outside it read them, from the
+    // kernel arguments
+    if (ROPE && !TABLE) {
+        for (int i = tid; i < HALF; i += kThreads) fstep[i] = a.fstep[i];
     }
+    const uint64_t* fsteps = TABLE ? a.fstep : fstep;
 
     // ---- queries: rotate at their positions, scale by softmax_scale*log2(e), bf16
     const int wave_row0 = row_lo + wave * 32;
@@ -317,14 +348,18 @@ __global__ void __launch_bounds__(kThreads, 1) prefill_bf16(const Plan plan, con
     const int hl = row_valid ? row - toff * G : 0;
     const int row_tok = row_valid ? g.tok0 + toff : t_last;
     bf16x8_t qb[KD];
-    {
-        __syncthreads();  // fstep ready
+    u32x4_t qraw[KD];
+    int32_t qpos = 0;
+    auto q_issue = [&]() {   // the queries' loads, issued before anything waits
         const uint16_t* qp = static_cast<const uint16_t*>(a.q) +
                              ((size_t)(g.q_row0 + toff) * a.hq + (size_t)kvh * G + hl) * D;
-        u32x4_t raw[KD];
 #pragma unroll
         for (int kd = 0; kd < KD; ++kd)
-            raw[kd] = row_valid ? *reinterpret_cast<const u32x4_t*>(qp + kd * 16 + 8 * hi) : u32x4_t{0, 0, 0, 0};
+            qraw[kd] = row_valid ? *reinterpret_cast<const u32x4_t*>(qp + kd * 16 + 8 * hi) : u32x4_t{0, 0, 0, 0};
+        if (ROPE && row_valid) qpos = a.positions[g.pos_off + g.tok0 + toff];
+    };
+    auto q_finish = [&]() {   // rotate, scale by softmax_scale*log2(e), round to bf16
+        const u32x4_t* raw = qraw;
         float xf[KD][8];
 #pragma unroll
         for (int kd = 0; kd < KD; ++kd)
@@ -334,12 +369,12 @@ __global__ void __launch_bounds__(kThreads, 1) prefill_bf16(const Plan plan, con
                 xf[kd][2 * m + 1] = bf_hi(raw[kd][m]);
             }
         if (ROPE) {
-            const int32_t pos = row_valid ? a.positions[g.pos_off + g.tok0 + toff] : 0;
+            const int32_t pos = qpos;
             if (STYLE == kNeox) {
 #pragma unroll
                 for (int kd = 0; kd < KD / 2; ++kd) {
                     float c[8], s[8];
-                    rope_cs_n<8, TABLE>(a.rope_table, a.rope_len, HALF, fstep, pos, kd * 16 + 8 * hi, c, s);
+                    rope_cs_n<8, TABLE>(a.rope_table, a.rope_len, HALF, fsteps, pos, kd * 16 + 8 * hi, c, s);
 #pragma unroll
                     for (int e = 0; e < 8; ++e) {
                         const float x = xf[kd][e], y = xf[kd + KD / 2][e];
@@ -351,7 +386,7 @@ __global__ void __launch_bounds__(kThreads, 1) prefill_bf16(const Plan plan, con
 #pragma unroll
                 for (int kd = 0; kd < KD; ++kd) {
                     float c[4], s[4];
-                    rope_cs_n<4, TABLE>(a.rope_table, a.rope_len, HALF, fstep, pos, kd * 8 + 4 * hi, c, s);
+                    rope_cs_n<4, TABLE>(a.rope_table, a.rope_len, HALF, fsteps, pos, kd * 8 + 4 * hi, c, s);
 #pragma unroll
                     for (int m = 0; m < 4; ++m) {
                         const float x = xf[kd][2 * m], y = xf[kd][2 * m + 1];
@@ -369,7 +404,7 @@ __global__ void __launch_bounds__(kThreads, 1) prefill_bf16(const Plan plan, con
                 w[m] = pack_bf16(xf[kd][2 * m] * a.scale_log2, xf[kd][2 * m + 1] * a.scale_log2);
             qb[kd] = __builtin_bit_cast(bf16x8_t, w);
         }
-    }
+    };
 
     f32x16_t acc[DB];
 #pragma unroll
@@ -380,10 +415,11 @@ __global__ void __launch_bounds__(kThreads, 1) prefill_bf16(const Plan plan, con
     const uint16_t* kpool = static_cast<const uint16_t*>(a.k_pool);
     const uint16_t* vpool = static_cast<const uint16_t*>(a.v_pool);
 
-    // staging role of this thread (K through registers when it is rotated): key kk of
-    // every tile, 16-element slice sc
+    // staging role of this thread (K through registers when it is rotated): keys
+    // kk + u * (kThreads / TPK), u < SU, of every tile, 16-element slice sc
     const bool stager = ROPE && tid < NSTAGE;
     const int kk = tid / TPK, sc = tid - (tid / TPK) * TPK;
+    constexpr int KSTEP = kThreads / TPK;
     const int kt0 = kv_lo & ~(kBlock - 1);
     const int n_tiles = (kv_hi - kt0 + BN - 1) / BN;
     // direct global->LDS role (V always, K too without RoPE): lane `lane` of wave
@@ -402,19 +438,22 @@ __global__ void __launch_bounds__(kThreads, 1) prefill_bf16(const Plan plan, con
     // of its key -- or, for keys outside [kv_lo, kv_hi), of the tile's first visible
     // key, so that no key outside the window is ever read (its score is masked).
     struct Meta {
-        int phys;
-        int32_t pos;
+        int phys[SU];
+        int32_t pos[SU];
         int dslot[DPW];
     };
     auto load_meta = [&](int t, Meta& m) {
         const int kt = kt0 + t * BN;
-        m.phys = 0;
-        m.pos = 0;
+#pragma unroll
+        for (int u = 0; u < SU; ++u) m.phys[u] = m.pos[u] = 0;
         if (t >= n_tiles) return;
-        const int j = kt + kk;
-        if (stager && j >= kv_lo && j < kv_hi) {
-            m.phys = btab[j >> 4];
-            m.pos = a.positions[g.pos_off + j];
+#pragma unroll
+        for (int u = 0; u < SU; ++u) {
+            const int j = kt + kk + u * KSTEP;
+            if (stager && j >= kv_lo && j < kv_hi) {
+                m.phys[u] = btab[j >> 4];
+                m.pos[u] = a.positions[g.pos_off + j];
+            }
         }
         const int j_ok = max(kt, kv_lo);
 #pragma unroll
@@ -433,14 +472,17 @@ __global__ void __launch_bounds__(kThreads, 1) prefill_bf16(const Plan plan, con
             if (!ROPE) global_to_lds16(kpool + row_off + dchunk(i) * 8, &ks[buf][lds_off]);
         }
     };
-    auto load_tile = [&](int t, const Meta& m, TileRegs& r) {
+    auto load_tile = [&](int t, const Meta& m, TileRegs* rr) {
         if (!stager) return;
-        const int j = kt0 + t * BN + kk;
+#pragma unroll
+        for (int u = 0; u < SU; ++u) {
+        TileRegs& r = rr[u];
+        const int j = kt0 + t * BN + kk + u * KSTEP;
         r.ok = j >= kv_lo && j < kv_hi;
-        r.pos = m.pos;
+        r.pos = m.pos[u];
         r.k[0] = r.k[1] = u32x4_t{0, 0, 0, 0};
         if (r.ok) {
-            const uint16_t* kp = kpool + (((size_t)m.phys * a.hkv + kvh) * kBlock + (j & 15)) * D;
+            const uint16_t* kp = kpool + (((size_t)m.phys[u] * a.hkv + kvh) * kBlock + (j & 15)) * D;
             if (STYLE == kNeox) {
                 r.k[0] = *reinterpret_cast<const u32x4_t*>(kp + sc * 8);
                 r.k[1] = *reinterpret_cast<const u32x4_t*>(kp + HALF + sc * 8);
@@ -448,15 +490,20 @@ __global__ void __launch_bounds__(kThreads, 1) prefill_bf16(const Plan plan, con
                 r.k[0] = *reinterpret_cast<const u32x4_t*>(kp + sc * 16);
                 r.k[1] = *reinterpret_cast<const u32x4_t*>(kp + sc * 16 + 8);
             }
-            if (TABLE && (uint32_t)m.pos < (uint32_t)a.rope_len) {
-                const float4* tp = reinterpret_cast<const float4*>(a.rope_table + ((size_t)m.pos * HALF + sc * 8) * 2);
+            if (TABLE && (uint32_t)r.pos < (uint32_t)a.rope_len) {
+                const float4* tp = reinterpret_cast<const float4*>(a.rope_table + ((size_t)r.pos * HALF + sc * 8) * 2);
 #pragma unroll
                 for (int k = 0; k < 4; ++k) r.cs[k] = tp[k];
             }
         }
+        }
     };
-    auto store_tile = [&](int buf, TileRegs& r) {
+    auto store_tile = [&](int buf, TileRegs* rr) {
         if (!stager) return;
+#pragma unroll
+        for (int u = 0; u < SU; ++u) {
+        TileRegs& r = rr[u];
+        const int kr = kk + u * KSTEP;
         // e[k] = (cos, -sin | sin, cos) of pair sc*8 + k as bf16: from the table, or
         // computed for keys whose position lies outside it (a wave-uniform branch, so
         // the common all-in-table case runs no fallback code)
@@ -472,7 +519,7 @@ __global__ void __launch_bounds__(kThreads, 1) prefill_bf16(const Plan plan, con
 #pragma unroll
                 for (int k = 0; k < 8; ++k) {
                     float c, sn;
-                    rope_cs(r.pos, fstep[sc * 8 + k], c, sn);
+                    rope_cs(r.pos, fsteps[sc * 8 + k], c, sn);
                     e[k] = bf16_entry(c, sn);
                 }
             }
@@ -502,20 +549,26 @@ __global__ void __launch_bounds__(kThreads, 1) prefill_bf16(const Plan plan, con
         if (__builtin_amdgcn_ballot_w64(!r.ok) != 0) {
             if (!r.ok) r.k[0] = r.k[1] = u32x4_t{0, 0, 0, 0};
         }
-        const int sw = swz<D>(kk);
-        uint16_t* krow = &ks[buf][kk * D];
+        const int sw = swz<D>(kr);
+        uint16_t* krow = &ks[buf][kr * D];
         const int ca = STYLE == kNeox ? sc : 2 * sc;
         const int cb = STYLE == kNeox ? sc + CH / 2 : 2 * sc + 1;
         *reinterpret_cast<u32x4_t*>(krow + ((ca ^ sw) << 3)) = r.k[0];
         *reinterpret_cast<u32x4_t*>(krow + ((cb ^ sw) << 3)) = r.k[1];
+        }
     };
 
-    TileRegs regs;
+    // ---- prologue: the queries' loads and the first tile's loads are all in flight
+    // before the first wait
+    TileRegs regs[SU];
     Meta meta_n, meta_nn;
+    q_issue();
     load_meta(0, meta_n);
     issue_direct(0, meta_n);
     load_tile(0, meta_n, regs);
     load_meta(1, meta_nn);
+    if (ROPE && !TABLE) __syncthreads();   // phase steps ready
+    q_finish();
     store_tile(0, regs);
     wait_vmem();
     __syncthreads();
@@ -557,7 +610,7 @@ __global__ void __launch_bounds__(kThreads, 1) prefill_bf16(const Plan plan, con
             // O^T += V^T P^T half; the second half's QK^T does not depend on the first
             // half's softmax, which leaves MFMA work to overlap with VALU work
 #pragma unroll
-            for (int mb = 0; mb < 2; ++mb) {
+            for (int mb = 0; mb < NH; ++mb) {
                 // ---- S^T (32 keys x 32 queries) = K Q^T
                 f32x16_t s = f32x16_t{};
 #pragma unroll
@@ -607,7 +660,7 @@ __global__ void __launch_bounds__(kThreads, 1) prefill_bf16(const Plan plan, con
                     }
                     pb[k2] = __builtin_bit_cast(bf16x8_t, w);
                 }
-                if (mb == 1 && more) load_tile(t + 1, meta_nn, regs);
+                if (mb == NH - 1 && more) load_tile(t + 1, meta_nn, regs);
                 // ---- O^T += V^T P^T
 #pragma unroll
                 for (int db = 0; db < DB; ++db)
@@ -650,7 +703,7 @@ __global__ void __launch_bounds__(kThreads, 1) prefill_bf16(const Plan plan, con
                 *reinterpret_cast<u32x2_t*>(op + d) = w;
             }
     } else {
-        const size_t slot = (size_t)g.part_base + (size_t)cluster * g.n_rt + rt;
+        const size_t slot = (size_t)part_base + (size_t)cluster * g.n_rt + rt;
         float* po = a.part_o + (slot * kTileRows + (row - row_lo)) * D;
 #pragma unroll
         for (int db = 0; db < DB; ++db)
@@ -676,10 +729,11 @@ __global__ void __launch_bounds__(kMergeRows * D / 4) merge_kernel(const Plan pl
     constexpr int TPR = D / 4;                      // threads per row
     constexpr int CHUNKS = kTileRows / kMergeRows;  // blocks per (row tile, KV head)
     constexpr int U = 8;                            // splits loaded per batch
-    const int gi = find_merge_group(plan, blockIdx.x);
+    int part_base = 0, merge_base = 0;
+    const int gi = find_merge_group(plan, blockIdx.x, a.hkv, part_base, merge_base);
     if (gi < 0) return;
     const Group g = plan.g[gi];
-    int li = blockIdx.x - g.merge_base;
+    int li = blockIdx.x - merge_base;
     if (li >= a.hkv * g.n_rt * CHUNKS) return;
     const int chunk = li % CHUNKS;
     li /= CHUNKS;
@@ -694,7 +748,7 @@ __global__ void __launch_bounds__(kMergeRows * D / 4) merge_kernel(const Plan pl
     const int r = chunk * kMergeRows + (int)threadIdx.x / TPR;
     const int q4 = (int)threadIdx.x % TPR;
     if (row_lo + r >= row_hi) return;
-    const size_t slot0 = (size_t)g.part_base + (size_t)kvh * g.n_split * g.n_rt + rt;
+    const size_t slot0 = (size_t)part_base + (size_t)kvh * g.n_split * g.n_rt + rt;
     float M = kNegBig, den = 0.f;
     float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
     for (int s0 = 0; s0 < n_live; s0 += U) {
@@ -741,7 +795,8 @@ __global__ void __launch_bounds__(64) attn_f32(const Plan plan, const Args a) {
     constexpr int HALF = D / 2;
     const int lane = threadIdx.x;
     const int bid = blockIdx.x;
-    const Group g = plan.g[find_group(plan, bid)];
+    int unused;
+    const Group g = plan.g[find_group(plan, bid, 0, unused)];
     const int li = bid - g.item_base;
     if (li >= g.n_tok * a.hq) return;
     const int toff = li / a.hq, h = li - toff * a.hq;
@@ -771,7 +826,7 @@ __global__ void __launch_bounds__(64) attn_f32(const Plan plan, const Args a) {
                 const float2 cs = reinterpret_cast<const float2*>(a.rope_table)[(size_t)pos * HALF + i];
                 c = cs.x; s = cs.y;
             } else {
-                rope_cs(pos, rope_phase_step(a.theta, i, D), c, s);
+                rope_cs(pos, a.fstep[i], c, s);
             }
             v[e] = first ? v[e] * c - pv[e] * s : v[e] * c + pv[e] * s;
         }
