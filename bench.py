@@ -14,6 +14,7 @@ bandwidth, and the fp64 CPU oracle on this host.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -61,6 +62,42 @@ def decode_bytes(wl) -> float:
     qo = 2.0 * wl.q.numel() * esize
     meta = 4.0 * float(np.sum(wl.seq_lens)) + 4.0 * wl.block_tables.size
     return kv + qo + meta
+
+
+KERNEL_SOURCES = ("paper_2606_13126_amd/csrc/pic_kernels.hip", "paper_2606_13126_amd/csrc/pic_host.cpp",
+                  "paper_2606_13126_amd/csrc/pic_internal.h")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_prefill_llama3_8b_rag.json")
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per attention call from the committed counter summary, if it was
+    taken on the current kernel sources (else None)."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("source_hash") != kernel_source_hash():
+        return None
+    return t.get("bytes_per_call")
+
+
+def calibration_copy(nbytes=256 << 20):
+    """A plain device copy of a known size: the reference dispatch for scaling the
+    FETCH_SIZE / WRITE_SIZE counters."""
+    x = torch.empty(nbytes // 2, dtype=torch.bfloat16, device="cuda").fill_(1.0)
+    y = torch.empty_like(x)
+    torch.cuda.synchronize()
+    y.copy_(x)
+    torch.cuda.synchronize()
 
 
 def timed(fn, steps, warmup, stream):
@@ -152,6 +189,7 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-extra", action="store_true")
     ap.add_argument("--configs", default="2,3,4")
+    ap.add_argument("--calib", action="store_true", help="also run the 256 MiB calibration copy")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (use --gpus 1)", file=sys.stderr)
@@ -195,11 +233,13 @@ def main():
                                "block 16, bf16",
                    "step": "pic_kv_write(256 rows) + pic_attn_prefill"},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
-                     "kernel": "pic_attn_prefill (prefill_bf16 + split merge)", "avg_ms": attn_avg},
+                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": measured_traffic(),
+                     "kernel": "pic_attn_prefill call (prefill_bf16 + split merge)", "avg_ms": attn_avg},
     }
     del db
     torch.cuda.empty_cache()
+    if args.calib:
+        calibration_copy()
     if not args.no_extra:
         extra = {"config1": bench_workload(wl, args.steps, args.warmup, stream)}
         for c in [int(x) for x in args.configs.split(",") if x]:
