@@ -99,6 +99,7 @@ pic_status check_batch(const pic_batch_host* b) {
 struct HostPlan {
     std::vector<pic::Group> groups;
     int64_t n_parts = 0;
+    bool dec_kernel = false;   // decode through the one-query kernel (bf16, G <= 16)
 };
 
 int32_t round_up(int64_t x, int64_t m) { return (int32_t)((x + m - 1) / m * m); }
@@ -143,7 +144,26 @@ pic_status make_plan(const pic_config* c, const pic_batch_host* b, bool decode, 
     }
     if (q_row > INT32_MAX / 2) return fail(PIC_EINVAL, "too many query rows");
 
-    if (c->dtype == PIC_F32) {
+    hp.dec_kernel = decode && c->dtype == PIC_BF16 && G <= pic::kDecMaxG;
+    if (hp.dec_kernel) {
+        // Decode items are (request, key split, group of 8 KV heads).  One workgroup
+        // holds a CU, so cut the keys into chunks of about the average work per CU
+        // (at least 4 cache blocks) and balance the splits of each request.
+        const int64_t n_hg = (c->num_kv_heads + pic::kDecGroupHeads - 1) / pic::kDecGroupHeads;
+        int64_t tiles_total = 0;
+        for (auto& g : hp.groups)
+            tiles_total += n_hg * (((int64_t)g.tok0 + 1 - g.win + pic::kDecTileKeys - 1) / pic::kDecTileKeys);
+        const int64_t chunk = std::max<int64_t>(4, (tiles_total + pic::kTargetCUs - 1) / pic::kTargetCUs);
+        for (auto& g : hp.groups) {
+            const int64_t tiles = ((int64_t)g.tok0 + 1 - g.win + pic::kDecTileKeys - 1) / pic::kDecTileKeys;
+            g.n_rt = 1;
+            g.n_split = (int32_t)((tiles + chunk - 1) / chunk);
+            g.split_keys = (int32_t)(((tiles + g.n_split - 1) / g.n_split) * pic::kDecTileKeys);
+        }
+        std::stable_sort(hp.groups.begin(), hp.groups.end(), [](const pic::Group& x, const pic::Group& y) {
+            return std::min<int64_t>(x.split_keys, x.tok0 + 1 - x.win) > std::min<int64_t>(y.split_keys, y.tok0 + 1 - y.win);
+        });
+    } else if (c->dtype == PIC_F32) {
         for (auto& g : hp.groups) {
             g.n_rt = g.n_tok;
             g.n_split = 1;
@@ -183,7 +203,12 @@ pic_status make_plan(const pic_config* c, const pic_batch_host* b, bool decode, 
     return PIC_OK;
 }
 
-int64_t items_of(const pic_config* c, const pic::Group& g) {
+int64_t dec_head_groups(const pic_config* c) {
+    return (c->num_kv_heads + pic::kDecGroupHeads - 1) / pic::kDecGroupHeads;
+}
+
+int64_t items_of(const pic_config* c, const HostPlan& hp, const pic::Group& g) {
+    if (hp.dec_kernel) return (int64_t)g.n_split * dec_head_groups(c);
     if (c->dtype == PIC_F32) return (int64_t)g.n_tok * c->num_q_heads;
     return (int64_t)g.n_rt * c->num_kv_heads * g.n_split;
 }
@@ -200,11 +225,17 @@ void make_launches(const pic_config* c, HostPlan& hp, std::vector<pic::Plan>& la
         int64_t item = 0, merge = 0;
         while (i < hp.groups.size() && p.n_groups < pic::kMaxGroups) {
             pic::Group g = hp.groups[i];
-            const int64_t n = items_of(c, g);
-            if (item + round_up(n, 8) > INT32_MAX / 2 && p.n_groups > 0) break;
+            const int64_t n = items_of(c, hp, g);
+            const int64_t n_pad = hp.dec_kernel ? n : round_up(n, 8);
+            if (item + n_pad > INT32_MAX / 2 && p.n_groups > 0) break;
             g.item_base = (int32_t)item;
-            item += round_up(n, 8);
-            if (c->dtype != PIC_F32 && g.n_split > 1) {
+            item += n_pad;
+            if (hp.dec_kernel) {
+                if (g.n_split > 1) {
+                    part += n;
+                    merge += (c->num_q_heads + pic::kMergeRows - 1) / pic::kMergeRows;
+                }
+            } else if (c->dtype != PIC_F32 && g.n_split > 1) {
                 part += (int64_t)g.n_rt * c->num_kv_heads * g.n_split;
                 merge += (int64_t)g.n_rt * c->num_kv_heads * (pic::kTileRows / pic::kMergeRows);
             }
@@ -288,7 +319,9 @@ pic_status run_attention(const pic_config* c, const pic_batch_host* b, const pic
     a.hkv = c->num_kv_heads;
     a.group = c->num_q_heads / c->num_kv_heads;
     for (const auto& p : launches) {
-        const int e = pic::launch_attention(c->dtype, c->rope_style, c->head_dim, c->k_prerotated == 0, p, a, stream);
+        const bool rope_on = c->k_prerotated == 0;
+        const int e = hp.dec_kernel ? pic::launch_decode(c->rope_style, c->head_dim, rope_on, p, a, stream)
+                                    : pic::launch_attention(c->dtype, c->rope_style, c->head_dim, rope_on, p, a, stream);
         if ((st = hip_status(e, "attention launch"))) return st;
     }
     return PIC_OK;
@@ -398,6 +431,21 @@ pic_status pic_plan_debug(const pic_config* cfg, const pic_batch_host* batch, in
         int64_t part_base = p.part0;
         for (int gi = 0; gi < p.n_groups; ++gi) {
             const pic::Group& g = p.g[gi];
+            if (hp.dec_kernel) {
+                const int64_t n_hg = dec_head_groups(cfg);
+                for (int s = 0; s < g.n_split; ++s) {
+                    const int32_t kl = g.win + s * g.split_keys;
+                    const int32_t kh = std::min(kl + g.split_keys, g.tok0 + 1);
+                    if (kl >= kh) continue;
+                    for (int kvh = 0; kvh < cfg->num_kv_heads; ++kvh) {
+                        const int32_t slot =
+                            g.n_split > 1 ? (int32_t)(part_base + s * n_hg + kvh / pic::kDecGroupHeads) : -1;
+                        emit(g.req, kvh, 0, G, kl, kh, g.tok0, slot);
+                    }
+                }
+                if (g.n_split > 1) part_base += g.n_split * n_hg;
+                continue;
+            }
             if (cfg->dtype == PIC_F32) {
                 for (int t = 0; t < g.n_tok; ++t)
                     for (int h = 0; h < cfg->num_q_heads; ++h) {

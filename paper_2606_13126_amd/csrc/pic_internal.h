@@ -19,6 +19,9 @@ constexpr int kTileKeys = PIC_TILE_KEYS;  // keys per K/V tile of the prefill ke
 constexpr int kMaxGroups = 72;    // groups passed by value in one launch (kernel arguments < 4 KB)
 constexpr int kTargetCUs = 256;   // MI355X compute units the split policy fills
 constexpr int kMergeRows = 8;     // rows per block of the split merge
+constexpr int kDecGroupHeads = 8; // KV heads per decode workgroup
+constexpr int kDecTileKeys = 16;  // keys per decode tile (one cache block)
+constexpr int kDecMaxG = 16;      // query heads per KV head the decode kernel handles
 
 // One query span of one request (prefill) or one request's last token (decode).
 // Its work items are (row tile, KV head, key split) triples, enumerated from
@@ -75,5 +78,6 @@ int launch_rope_table(int dtype, int d, double theta, int n_pos, float* table, v
 int launch_rope_rotate(int dtype, int style, int d, double theta, const float* table, int rope_len, void* x,
                        int n, int heads, const int32_t* positions, void* stream);
 int launch_attention(int dtype, int style, int d, bool rope, const Plan& plan, const Args& args, void* stream);
+int launch_decode(int style, int d, bool rope, const Plan& plan, const Args& args, void* stream);
 
 }  // namespace pic

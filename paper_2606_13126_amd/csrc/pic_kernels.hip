@@ -787,6 +787,420 @@ __global__ void __launch_bounds__(kMergeRows * D / 4) merge_kernel(const Plan pl
 }
 
 // ---------------------------------------------------------------------------------
+// decode_bf16
+//
+// One query per (request, query head).  Workgroup = (request, key split, group of
+// up to 8 KV heads); wave w owns KV head 8*hg + w and its G <= 16 query heads as
+// the 16 columns of 16x16 MFMA tiles.  Tiles are 16 keys = one cache block, so a
+// tile's K or V for the 8 heads is one contiguous 32 KB run of the pool.
+//   S^T (16 keys x 16 queries) = K Q^T    v_mfma_f32_16x16x32_bf16, K from LDS
+//   O^T (16 dims x 16 queries) += V^T P^T v_mfma_f32_16x16x16_bf16, V^T through
+//                                          ds_read_b64_tr_b16
+// After QK^T lane l holds query l%16 and keys 4*(l/16) + {0..3}, which is exactly
+// the B operand of the PV step, so probabilities never leave their lanes; row
+// statistics need two exchanges (lanes l^16 and l^32).
+// ---------------------------------------------------------------------------------
+constexpr int kDecHeads = 8;     // KV heads (waves) per decode workgroup
+constexpr int kDecKeys = 16;     // keys per decode tile
+
+__device__ __forceinline__ int dec_parts(const Group& x, int n_hg) { return x.n_split > 1 ? x.n_split * n_hg : 0; }
+
+__device__ __forceinline__ int find_dec_group(const Plan& plan, int bid, int n_hg, int& part_base) {
+    int gi = 0, part = plan.part0;
+    while (gi + 1 < plan.n_groups && plan.g[gi + 1].item_base <= bid) {
+        part += dec_parts(plan.g[gi], n_hg);
+        ++gi;
+    }
+    part_base = part;
+    return gi;
+}
+
+__device__ __forceinline__ float max_xor16(float x) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_xor16(float x) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+template <int D, int STYLE, bool ROPE, bool TABLE>
+__global__ void __launch_bounds__(kDecHeads * 64, 1) decode_bf16(const Plan plan, const Args a) {
+    typedef float f32x4_t __attribute__((ext_vector_type(4)));
+    typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+    constexpr int KD = D / 32;            // 16x16x32 contraction steps of QK^T
+    constexpr int DB = D / 16;            // 16-dim blocks of O^T
+    constexpr int CH = D / 8;             // 16-byte chunks per row
+    constexpr int HALF = D / 2;
+    constexpr int TK = kDecKeys;
+    constexpr int HW = kDecHeads;
+    constexpr int NT = HW * 64;           // threads
+    constexpr int TPK = D / 16;           // staging threads per (head, key)
+    constexpr int SU = HW * TK * TPK / NT; // staged (head, key) slices per thread
+    constexpr int HSZ = TK * D;           // elements of one head's tile
+    constexpr int DPL = HW * HSZ / 8 / NT; // direct 16-byte loads per lane per tile
+    static_assert(SU >= 1 && DPL >= 1, "decode tile shape");
+
+    __shared__ __attribute__((aligned(16))) uint16_t ks[2][HW * HSZ];
+    __shared__ __attribute__((aligned(16))) uint16_t vs[2][HW * HSZ];
+    __shared__ uint64_t fstep[HALF];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int c16 = lane & 15, q4 = lane >> 4;   // MFMA column (query) and row group
+    const int n_hg = (a.hkv + HW - 1) / HW;
+    int part_base;
+    const Group g = plan.g[find_dec_group(plan, blockIdx.x, n_hg, part_base)];
+    const int li = blockIdx.x - g.item_base;
+    if (li >= g.n_split * n_hg) return;
+    const int split = li / n_hg, hg = li - (li / n_hg) * n_hg;
+    const int G = a.group;
+    const int L = g.tok0 + 1;                    // keys of the request (the query is its last token)
+    const int kv_lo = g.win + split * g.split_keys;
+    const int kv_hi = min(kv_lo + g.split_keys, L);
+    if (kv_lo >= kv_hi) return;
+    const int kvh = hg * HW + wave;              // this wave's KV head
+    const bool head_live = kvh < a.hkv;
+    const int n_heads_here = min(HW, a.hkv - hg * HW);
+
+    if (ROPE && !TABLE)
+        for (int i = tid; i < HALF; i += NT) fstep[i] = a.fstep[i];
+    const uint64_t* fsteps = TABLE ? a.fstep : fstep;
+
+    const int32_t* btab = a.block_tables + (size_t)g.req * a.max_blocks;
+    const uint16_t* kpool = static_cast<const uint16_t*>(a.k_pool);
+    const uint16_t* vpool = static_cast<const uint16_t*>(a.v_pool);
+    const int kt0 = kv_lo & ~(TK - 1);
+    const int n_tiles = (kv_hi - kt0 + TK - 1) / TK;
+
+    // ---- staging roles: slice sc of key kk of head hh (u-th unit of the thread)
+    auto unit = [&](int u, int& hh, int& kk, int& sc) {
+        const int x = tid + u * NT;
+        hh = x / (TK * TPK);
+        kk = (x / TPK) % TK;
+        sc = x % TPK;
+    };
+    struct Regs {
+        u32x4_t k[SU][2];
+        float4 cs[SU][4];
+        int32_t pos[SU];
+    };
+    int32_t next_pos[SU];  // positions of the staged keys, read one tile ahead
+    Regs regs;
+
+    // keys outside [kv_lo, kv_hi) are loaded from the tile's first visible key, so
+    // that nothing outside the window is read (their scores are masked)
+    auto clamp_key = [&](int kt, int j) { return (j >= kv_lo && j < kv_hi) ? j : max(kt, kv_lo); };
+
+    // ---- queries: B operand of S^T = K Q^T, rotated at the last token's position
+    bf16x8_t qb[KD];
+    {
+        const bool qv = head_live && c16 < G;
+        const int qh = kvh * G + c16;
+        const uint16_t* qp = static_cast<const uint16_t*>(a.q) + ((size_t)g.q_row0 * a.hq + qh) * D;
+        float xf[KD][8];
+#pragma unroll
+        for (int kd = 0; kd < KD; ++kd) {
+            const u32x4_t raw = qv ? *reinterpret_cast<const u32x4_t*>(qp + kd * 32 + 8 * q4) : u32x4_t{0, 0, 0, 0};
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+                xf[kd][2 * m] = bf_lo(raw[m]);
+                xf[kd][2 * m + 1] = bf_hi(raw[m]);
+            }
+        }
+        if (ROPE) {
+            if (!TABLE) __syncthreads();   // phase steps in LDS
+            const int32_t pos = a.positions[g.pos_off + g.tok0];
+            if (STYLE == kNeox) {
+#pragma unroll
+                for (int kd = 0; kd < KD / 2; ++kd) {
+                    float c[8], sn[8];
+                    rope_cs_n<8, TABLE>(a.rope_table, a.rope_len, HALF, fsteps, pos, kd * 32 + 8 * q4, c, sn);
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const float x = xf[kd][e], y = xf[kd + KD / 2][e];
+                        xf[kd][e] = x * c[e] - y * sn[e];
+                        xf[kd + KD / 2][e] = y * c[e] + x * sn[e];
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int kd = 0; kd < KD; ++kd) {
+                    float c[4], sn[4];
+                    rope_cs_n<4, TABLE>(a.rope_table, a.rope_len, HALF, fsteps, pos, kd * 16 + 4 * q4, c, sn);
+#pragma unroll
+                    for (int m = 0; m < 4; ++m) {
+                        const float x = xf[kd][2 * m], y = xf[kd][2 * m + 1];
+                        xf[kd][2 * m] = x * c[m] - y * sn[m];
+                        xf[kd][2 * m + 1] = y * c[m] + x * sn[m];
+                    }
+                }
+            }
+        }
+#pragma unroll
+        for (int kd = 0; kd < KD; ++kd) {
+            u32x4_t w;
+#pragma unroll
+            for (int m = 0; m < 4; ++m)
+                w[m] = pack_bf16(xf[kd][2 * m] * a.scale_log2, xf[kd][2 * m + 1] * a.scale_log2);
+            qb[kd] = __builtin_bit_cast(bf16x8_t, w);
+        }
+    }
+
+    // ---- loads of one tile: positions one tile ahead, K slices into registers
+    // (rotated on their way to LDS), V straight into LDS
+    auto load_pos = [&](int t) {
+        if (!ROPE) return;
+#pragma unroll
+        for (int u = 0; u < SU; ++u) {
+            int hh, kk, sc;
+            unit(u, hh, kk, sc);
+            const int j = kt0 + t * TK + kk;
+            next_pos[u] = (ROPE && t < n_tiles && j < kv_hi && j >= kv_lo) ? a.positions[g.pos_off + j] : 0;
+        }
+    };
+    auto issue_tile = [&](int t, int buf) {
+        const int kt = kt0 + t * TK;
+        const int blk = btab[kt >> 4];   // the tile is exactly one block
+#pragma unroll
+        for (int u = 0; u < SU && ROPE; ++u) {
+            int hh, kk, sc;
+            unit(u, hh, kk, sc);
+            const int j = clamp_key(kt, kt + kk);
+            const int hs = min(hh, n_heads_here - 1);   // heads past Hkv load a real head, never read
+            const uint16_t* kp = kpool + (((size_t)blk * a.hkv + hg * HW + hs) * kBlock + (j & 15)) * D;
+            regs.pos[u] = next_pos[u];
+            if (STYLE == kNeox) {
+                regs.k[u][0] = *reinterpret_cast<const u32x4_t*>(kp + sc * 8);
+                regs.k[u][1] = *reinterpret_cast<const u32x4_t*>(kp + HALF + sc * 8);
+            } else {
+                regs.k[u][0] = *reinterpret_cast<const u32x4_t*>(kp + sc * 16);
+                regs.k[u][1] = *reinterpret_cast<const u32x4_t*>(kp + sc * 16 + 8);
+            }
+            if (ROPE && TABLE && (uint32_t)regs.pos[u] < (uint32_t)a.rope_len) {
+                const float4* tp =
+                    reinterpret_cast<const float4*>(a.rope_table + ((size_t)regs.pos[u] * HALF + sc * 8) * 2);
+#pragma unroll
+                for (int k = 0; k < 4; ++k) regs.cs[u][k] = tp[k];
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < DPL; ++i) {
+            const int p = (i * HW + wave) * 64 + lane;   // 16-byte chunk of the V tile
+            const int hh = p / (HSZ / 8), q = p % (HSZ / 8);
+            const int kk = q / CH, pc = q % CH;
+            const int j = clamp_key(kt, kt + kk);
+            const int hs = min(hh, n_heads_here - 1);
+            const size_t off = (((size_t)blk * a.hkv + hg * HW + hs) * kBlock + (j & 15)) * D + ((pc ^ swz<D>(kk)) << 3);
+            global_to_lds16(vpool + off, &vs[buf][(i * HW + wave) * 64 * 8]);
+            if (!ROPE) global_to_lds16(kpool + off, &ks[buf][(i * HW + wave) * 64 * 8]);
+        }
+    };
+    auto store_k = [&](int t, int buf) {
+        if (!ROPE) return;   // pre-rotated K went straight to LDS
+        const int kt = kt0 + t * TK;
+#pragma unroll
+        for (int u = 0; u < SU; ++u) {
+            int hh, kk, sc;
+            unit(u, hh, kk, sc);
+            const int j = kt + kk;
+            const bool ok = j >= kv_lo && j < kv_hi;
+            u32x4_t k0 = regs.k[u][0], k1 = regs.k[u][1];
+            if (ROPE) {
+                uint2 e[8];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    e[2 * k] = make_uint2(__float_as_uint(regs.cs[u][k].x), __float_as_uint(regs.cs[u][k].y));
+                    e[2 * k + 1] = make_uint2(__float_as_uint(regs.cs[u][k].z), __float_as_uint(regs.cs[u][k].w));
+                }
+                const bool need_cs = ok && !(TABLE && (uint32_t)regs.pos[u] < (uint32_t)a.rope_len);
+                if (!TABLE || __builtin_amdgcn_ballot_w64(need_cs) != 0) {
+                    if (need_cs) {
+#pragma unroll
+                        for (int k = 0; k < 8; ++k) {
+                            float c, sn;
+                            rope_cs(regs.pos[u], fsteps[sc * 8 + k], c, sn);
+                            e[k] = bf16_entry(c, sn);
+                        }
+                    }
+                }
+                if (STYLE == kNeox) {
+#pragma unroll
+                    for (int m = 0; m < 4; ++m) {
+                        const uint32_t A = k0[m], B = k1[m];
+                        const uint32_t p0 = (A & 0xffffu) | (B << 16), p1 = (A >> 16) | (B & 0xffff0000u);
+                        k0[m] = pack_bf16(dot2_bf16(p0, e[2 * m].x), dot2_bf16(p1, e[2 * m + 1].x));
+                        k1[m] = pack_bf16(dot2_bf16(p0, e[2 * m].y), dot2_bf16(p1, e[2 * m + 1].y));
+                    }
+                } else {
+#pragma unroll
+                    for (int m = 0; m < 4; ++m) {
+                        k0[m] = pack_bf16(dot2_bf16(k0[m], e[m].x), dot2_bf16(k0[m], e[m].y));
+                        k1[m] = pack_bf16(dot2_bf16(k1[m], e[4 + m].x), dot2_bf16(k1[m], e[4 + m].y));
+                    }
+                }
+            }
+            if (!ok) k0 = k1 = u32x4_t{0, 0, 0, 0};
+            uint16_t* row = &ks[buf][hh * HSZ + kk * D];
+            const int sw = swz<D>(kk);
+            const int ca = STYLE == kNeox ? sc : 2 * sc, cb = STYLE == kNeox ? sc + CH / 2 : 2 * sc + 1;
+            *reinterpret_cast<u32x4_t*>(row + ((ca ^ sw) << 3)) = k0;
+            *reinterpret_cast<u32x4_t*>(row + ((cb ^ sw) << 3)) = k1;
+        }
+    };
+
+    f32x4_t acc[DB];
+#pragma unroll
+    for (int db = 0; db < DB; ++db) acc[db] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    float m_run = kNegBig, l_run = 0.f;
+
+    // per-lane LDS offsets within one head's tile
+    int k_off[KD];
+#pragma unroll
+    for (int kd = 0; kd < KD; ++kd) k_off[kd] = c16 * D + (((kd * 4 + q4) ^ swz<D>(c16)) << 3);
+    int v_off[DB];
+    {
+        const int key = 4 * q4 + ((lane & 15) >> 2);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+            const int d = db * 16 + 4 * (lane & 3);
+            v_off[db] = key * D + (((d >> 3) ^ swz<D>(key)) << 3) + (d & 7);
+        }
+    }
+
+    load_pos(0);
+    issue_tile(0, 0);
+    load_pos(1);
+    store_k(0, 0);
+    wait_vmem();
+    __syncthreads();
+
+    for (int t = 0; t < n_tiles; ++t) {
+        const int buf = t & 1;
+        const int kt = kt0 + t * TK;
+        const bool more = t + 1 < n_tiles;
+        if (more) {
+            issue_tile(t + 1, buf ^ 1);
+            load_pos(t + 2);
+        }
+        if (head_live) {
+            const uint16_t* kb = &ks[buf][wave * HSZ];
+            lds_u16_t* vb = as_lds(&vs[buf][wave * HSZ]);
+            f32x4_t sc4 = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int kd = 0; kd < KD; ++kd) {
+                const bf16x8_t af = *reinterpret_cast<const bf16x8_t*>(kb + k_off[kd]);
+                sc4 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, qb[kd], sc4, 0, 0, 0);
+            }
+            if (kt < kv_lo || kt + TK > kv_hi) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int key = kt + 4 * q4 + r;
+                    if (key < kv_lo || key >= kv_hi) sc4[r] = -INFINITY;
+                }
+            }
+            float mx = fmaxf(fmaxf(sc4[0], sc4[1]), fmaxf(sc4[2], sc4[3]));
+            mx = max_xor32(max_xor16(mx));
+            if (__builtin_amdgcn_ballot_w64(mx > m_run + 8.f) != 0) {
+                const float m_new = fmaxf(m_run, mx);
+                const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+                l_run *= alpha;
+#pragma unroll
+                for (int db = 0; db < DB; ++db) acc[db] *= alpha;
+                m_run = m_new;
+            }
+            float p[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                p[r] = __builtin_amdgcn_exp2f(sc4[r] - m_run);
+                l_run += p[r];
+            }
+            const uint32_t pw[2] = {pack_bf16(p[0], p[1]), pack_bf16(p[2], p[3])};
+            const bf16x4_t pb = __builtin_bit_cast(bf16x4_t, pw);
+#pragma unroll
+            for (int db = 0; db < DB; ++db) {
+                const bf16x4_t af = __builtin_bit_cast(bf16x4_t, lds_read_tr(vb + v_off[db]));
+                acc[db] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(af, pb, acc[db], 0, 0, 0);
+            }
+        }
+        if (more) store_k(t + 1, buf ^ 1);
+        wait_vmem();
+        __syncthreads();
+    }
+
+    // ---- epilogue: lane l holds query column l%16 and dims 16*db + 4*(l/16) + r
+    const float lt = sum_xor32(sum_xor16(l_run));
+    if (!head_live || c16 >= G) return;
+    const int qh = kvh * G + c16;
+    if (g.n_split == 1) {
+        const float inv = 1.f / lt;
+        uint16_t* op = static_cast<uint16_t*>(a.o) + ((size_t)g.q_row0 * a.hq + qh) * D;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+            const u32x2_t w = {pack_bf16(acc[db][0] * inv, acc[db][1] * inv), pack_bf16(acc[db][2] * inv, acc[db][3] * inv)};
+            *reinterpret_cast<u32x2_t*>(op + db * 16 + 4 * q4) = w;
+        }
+    } else {
+        const size_t slot = (size_t)part_base + (size_t)split * n_hg + hg;
+        const int prow = wave * 16 + c16;
+        float* po = a.part_o + (slot * kTileRows + prow) * D;
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+            *reinterpret_cast<float4*>(po + db * 16 + 4 * q4) = make_float4(acc[db][0], acc[db][1], acc[db][2], acc[db][3]);
+        if (q4 == 0)
+            *reinterpret_cast<float2*>(a.part_ml + (slot * kTileRows + prow) * 2) = make_float2(m_run, lt);
+    }
+}
+
+// decode merge: one block per (request, 8 query heads), one float4 of a row per thread
+template <int D>
+__global__ void __launch_bounds__(kMergeRows * D / 4) decode_merge(const Plan plan, const Args a) {
+    constexpr int TPR = D / 4;
+    const int n_hg = (a.hkv + kDecHeads - 1) / kDecHeads;
+    const int per_req = (a.hq + kMergeRows - 1) / kMergeRows;
+    // locate the request among the split groups
+    int part = plan.part0, merge = 0, gi = -1;
+    for (int i = 0; i < plan.n_groups; ++i) {
+        const int nb = plan.g[i].n_split > 1 ? per_req : 0;
+        if ((int)blockIdx.x < merge + nb) {
+            gi = i;
+            break;
+        }
+        merge += nb;
+        part += dec_parts(plan.g[i], n_hg);
+    }
+    if (gi < 0) return;
+    const Group g = plan.g[gi];
+    const int qh = ((int)blockIdx.x - merge) * kMergeRows + (int)threadIdx.x / TPR;
+    const int q4 = (int)threadIdx.x % TPR;
+    if (qh >= a.hq) return;
+    const int kvh = qh / a.group, c = qh - kvh * a.group;
+    const int hg = kvh / kDecHeads, prow = (kvh % kDecHeads) * 16 + c;
+    const int L = g.tok0 + 1;
+    float M = kNegBig, den = 0.f;
+    float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int s = 0; s < g.n_split; ++s) {
+        if (g.win + s * g.split_keys >= L) break;
+        const size_t slot = (size_t)part + (size_t)s * n_hg + hg;
+        const float2 ml = *reinterpret_cast<const float2*>(a.part_ml + (slot * kTileRows + prow) * 2);
+        if (!(ml.y > 0.f)) continue;
+        const float4 v = *reinterpret_cast<const float4*>(a.part_o + (slot * kTileRows + prow) * D + q4 * 4);
+        const float m_new = fmaxf(M, ml.x);
+        const float c_old = __builtin_amdgcn_exp2f(M - m_new), c_new = __builtin_amdgcn_exp2f(ml.x - m_new);
+        num.x = num.x * c_old + c_new * v.x;
+        num.y = num.y * c_old + c_new * v.y;
+        num.z = num.z * c_old + c_new * v.z;
+        num.w = num.w * c_old + c_new * v.w;
+        den = den * c_old + c_new * ml.y;
+        M = m_new;
+    }
+    const float inv = 1.f / den;
+    uint32_t* op = reinterpret_cast<uint32_t*>(static_cast<uint16_t*>(a.o) + ((size_t)g.q_row0 * a.hq + qh) * D + q4 * 4);
+    op[0] = pack_bf16(num.x * inv, num.y * inv);
+    op[1] = pack_bf16(num.z * inv, num.w * inv);
+}
+
+// ---------------------------------------------------------------------------------
 // attn_f32: one wave per (query token, query head); lane holds D/64 elements.
 // ---------------------------------------------------------------------------------
 template <int D, int STYLE, bool ROPE, bool TABLE>
@@ -889,6 +1303,25 @@ hipError_t launch_attn_t(int dtype, const Plan& plan, const Args& a, hipStream_t
     return e;
 }
 
+template <int D, int STYLE, bool ROPE, bool TABLE>
+hipError_t launch_dec_t(const Plan& plan, const Args& a, hipStream_t st) {
+    hipLaunchKernelGGL((decode_bf16<D, STYLE, ROPE, TABLE>), dim3(plan.n_items), dim3(kDecHeads * 64), 0, st, plan, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (plan.n_merge > 0) {
+        hipLaunchKernelGGL((decode_merge<D>), dim3(plan.n_merge), dim3(kMergeRows * D / 4), 0, st, plan, a);
+        e = hipGetLastError();
+    }
+    return e;
+}
+
+template <int D, int STYLE>
+hipError_t launch_dec_d(bool rope, const Plan& plan, const Args& a, hipStream_t st) {
+    const bool table = a.rope_table != nullptr && a.rope_len > 0;
+    if (!rope) return launch_dec_t<D, STYLE, false, false>(plan, a, st);
+    return table ? launch_dec_t<D, STYLE, true, true>(plan, a, st) : launch_dec_t<D, STYLE, true, false>(plan, a, st);
+}
+
 template <int D, int STYLE>
 hipError_t launch_attn_d(int dtype, bool rope, const Plan& plan, const Args& a, hipStream_t st) {
     const bool table = a.rope_table != nullptr && a.rope_len > 0;
@@ -944,6 +1377,14 @@ int launch_rope_rotate(int dtype, int style, int d, double theta, const float* t
                                n_pairs, heads, d, theta, positions, t, rope_len);
     }
     return hipGetLastError();
+}
+
+int launch_decode(int style, int d, bool rope, const Plan& plan, const Args& args, void* stream) {
+    if (plan.n_items == 0) return hipSuccess;
+    hipStream_t st = (hipStream_t)stream;
+    if (d == 64)
+        return style == kNeox ? launch_dec_d<64, 0>(rope, plan, args, st) : launch_dec_d<64, 1>(rope, plan, args, st);
+    return style == kNeox ? launch_dec_d<128, 0>(rope, plan, args, st) : launch_dec_d<128, 1>(rope, plan, args, st);
 }
 
 int launch_attention(int dtype, int style, int d, bool rope, const Plan& plan, const Args& args, void* stream) {

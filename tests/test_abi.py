@@ -195,3 +195,22 @@ def test_plan_pair_count_large(cfg_i):
         total += np.clip(np.minimum(kh, t + 1) - kl, 0, None).sum()
     pairs = O.visible_pairs(wl.seq_lens, wl.cu_spans, wl.span_start, wl.span_flags)
     assert total == pairs * wl.num_q_heads
+
+
+@pytest.mark.parametrize("Hq,Hkv,D", [(8, 8, 64), (16, 16, 64), (40, 10, 128), (32, 2, 128), (34, 2, 64)])
+def test_plan_exact_cover_decode_shapes(Hq, Hkv, D):
+    from tests.cases import decode_case
+    wl = decode_case(Hq, Hkv, D, seed=1)
+    G = Hq // Hkv
+    assert check_exact_cover(wl, B.PIC_BF16, True) == wl.num_reqs * Hkv * G
+    # split partial slots are distinct per (split, head group) and dense from 0
+    cfg = P.make_config(Hq, Hkv, D)
+    items = P.pic_plan_debug(cfg, batch_of(wl), True)
+    slots = {}
+    for req, kvh, rl, rh, kl, kh, tok0, slot in items:
+        if slot >= 0:
+            slots.setdefault(int(slot), set()).add((int(req), int(kl), int(kvh) // 8 if G <= 16 else int(kvh)))
+    for s, owners in slots.items():
+        assert len({(r, k) for r, k, _ in owners}) == 1, (s, owners)
+    if slots:
+        assert sorted(slots) == list(range(len(slots)))

@@ -6,6 +6,7 @@ import torch
 import workloads as W
 from oracle import pic_oracle as O
 from oracle import workload_oracle as WO
+from tests.cases import decode_case
 from tests.gpu_util import assert_close, gpu_run, say, to_np
 
 pytestmark = pytest.mark.gpu
@@ -217,3 +218,48 @@ def test_rope_table_accuracy():
     for k, ref in ((0, np.cos(p)), (2, np.sin(p))):
         ulp = np.exp2(np.floor(np.log2(np.maximum(np.abs(ref), 1e-30))) - 7)
         assert np.all(np.abs(got[..., k] - ref) <= ulp)
+
+
+@pytest.mark.parametrize("Hq,Hkv,D,style,table_len", [
+    (8, 8, 64, 0, None),        # MHA, one full group of 8 KV heads
+    (16, 16, 64, 1, 0),         # MHA, two head groups, computed cos/sin only
+    (40, 10, 128, 0, 2000),     # G = 4, a partial second head group, table + computed
+    (32, 2, 128, 1, None),      # G = 16, the widest query group of one MFMA tile
+    (34, 2, 64, 0, None),       # G = 17: the general kernel takes it
+])
+def test_decode_head_groups_and_windows(Hq, Hkv, D, style, table_len):
+    wl = decode_case(Hq, Hkv, D, seed=20 + Hq)
+    say(f"[gpu] decode Hq={Hq} Hkv={Hkv} D={D} style={style} table_len={table_len}")
+    db = gpu_run(wl, rope_style=style, table=table_len != 0, table_len=table_len or None)
+    assert_close(to_np(db.o), WO.run(wl, style="neox" if style == 0 else "gptj"), wl.dtype, wl.name)
+
+
+def test_decode_prerotated_equals_fused():
+    # the k_prerotated variant of the decode kernel (the RoPE-cost baseline) gives
+    # the fused result when K and q are rotated beforehand (private spans only)
+    import paper_2606_13126_amd as P
+    from paper_2606_13126_amd.runner import DeviceBatch
+    reqs = [[Sp(37, S), Sp(5, S, fresh=True)], [Sp(333, Pd), Sp(1, Pd, fresh=True)], [Sp(64, S), Sp(9, 0, fresh=True)]]
+    wl = W.small_case("decode_pre", reqs, Hq=32, Hkv=8, D=128, theta=5e5, dtype=torch.bfloat16, seed=31,
+                      value_scale=0.5, decode=True, position_offsets=[3, 900, 17])
+    fused = gpu_run(wl)
+    ctl = DeviceBatch(wl, k_prerotated=True, table_positions=int(wl.positions.max()) + 1)
+    ctl.write()
+    kp = ctl.k_pool.permute(0, 2, 1, 3).reshape(-1, wl.num_kv_heads, wl.head_dim)
+    off = wl.seq_offsets
+    qpos = []
+    for r in range(wl.num_reqs):
+        L = int(wl.seq_lens[r])
+        n = torch.arange(L)
+        slots = (torch.from_numpy(wl.block_tables[r].astype(np.int64))[n // 16] * 16 + n % 16).cuda()
+        pos = torch.from_numpy(wl.positions[off[r]:off[r + 1]]).cuda()
+        rows = kp[slots].contiguous()
+        P.pic_rope_rotate(ctl.cfg, rows, pos, table=ctl.table)
+        kp[slots] = rows
+        qpos.append(int(wl.positions[off[r] + L - 1]))
+    ctl.k_pool = kp.reshape(-1, 16, wl.num_kv_heads, wl.head_dim).permute(0, 2, 1, 3).contiguous()
+    P.pic_rope_rotate(ctl.cfg, ctl.q, torch.tensor(qpos, dtype=torch.int32, device="cuda"), table=ctl.table)
+    ctl.attend()
+    torch.cuda.synchronize()
+    assert_close(to_np(ctl.o), to_np(fused.o), wl.dtype, "pre-rotated decode vs fused")
+    assert_close(to_np(fused.o), WO.run(wl), wl.dtype, "fused decode vs oracle")
