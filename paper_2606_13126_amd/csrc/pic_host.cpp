@@ -146,10 +146,11 @@ pic_status make_plan(const pic_config* c, const pic_batch_host* b, bool decode, 
 
     hp.dec_kernel = decode && c->dtype == PIC_BF16 && G <= pic::kDecMaxG;
     if (hp.dec_kernel) {
-        // Decode items are (request, key split, group of 8 KV heads).  One workgroup
+        // Decode items are (request, key split, group of KV heads).  One workgroup
         // holds a CU, so cut the keys into chunks of about the average work per CU
         // (at least 4 cache blocks) and balance the splits of each request.
-        const int64_t n_hg = (c->num_kv_heads + pic::kDecGroupHeads - 1) / pic::kDecGroupHeads;
+        const int64_t hw = pic::dec_heads(c->head_dim);
+        const int64_t n_hg = (c->num_kv_heads + hw - 1) / hw;
         int64_t tiles_total = 0;
         for (auto& g : hp.groups)
             tiles_total += n_hg * (((int64_t)g.tok0 + 1 - g.win + pic::kDecTileKeys - 1) / pic::kDecTileKeys);
@@ -204,7 +205,7 @@ pic_status make_plan(const pic_config* c, const pic_batch_host* b, bool decode, 
 }
 
 int64_t dec_head_groups(const pic_config* c) {
-    return (c->num_kv_heads + pic::kDecGroupHeads - 1) / pic::kDecGroupHeads;
+    return (c->num_kv_heads + pic::dec_heads(c->head_dim) - 1) / pic::dec_heads(c->head_dim);
 }
 
 int64_t items_of(const pic_config* c, const HostPlan& hp, const pic::Group& g) {
@@ -439,7 +440,7 @@ pic_status pic_plan_debug(const pic_config* cfg, const pic_batch_host* batch, in
                     if (kl >= kh) continue;
                     for (int kvh = 0; kvh < cfg->num_kv_heads; ++kvh) {
                         const int32_t slot =
-                            g.n_split > 1 ? (int32_t)(part_base + s * n_hg + kvh / pic::kDecGroupHeads) : -1;
+                            g.n_split > 1 ? (int32_t)(part_base + s * n_hg + kvh / pic::dec_heads(cfg->head_dim)) : -1;
                         emit(g.req, kvh, 0, G, kl, kh, g.tok0, slot);
                     }
                 }

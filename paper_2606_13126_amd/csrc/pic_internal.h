@@ -19,9 +19,13 @@ constexpr int kTileKeys = PIC_TILE_KEYS;  // keys per K/V tile of the prefill ke
 constexpr int kMaxGroups = 72;    // groups passed by value in one launch (kernel arguments < 4 KB)
 constexpr int kTargetCUs = 256;   // MI355X compute units the split policy fills
 constexpr int kMergeRows = 8;     // rows per block of the split merge
-constexpr int kDecGroupHeads = 8; // KV heads per decode workgroup
 constexpr int kDecTileKeys = 16;  // keys per decode tile (one cache block)
 constexpr int kDecMaxG = 16;      // query heads per KV head the decode kernel handles
+#ifndef PIC_DEC_HEADS_D128
+#define PIC_DEC_HEADS_D128 8
+#endif
+// KV heads per decode workgroup (one wave each)
+constexpr int dec_heads(int head_dim) { return head_dim == 128 ? PIC_DEC_HEADS_D128 : 8; }
 
 // One query span of one request (prefill) or one request's last token (decode).
 // Its work items are (row tile, KV head, key split) triples, enumerated from

@@ -787,21 +787,9 @@ __global__ void __launch_bounds__(kMergeRows * D / 4) merge_kernel(const Plan pl
 }
 
 // ---------------------------------------------------------------------------------
-// decode_bf16
-//
-// One query per (request, query head).  Workgroup = (request, key split, group of
-// up to 8 KV heads); wave w owns KV head 8*hg + w and its G <= 16 query heads as
-// the 16 columns of 16x16 MFMA tiles.  Tiles are 16 keys = one cache block, so a
-// tile's K or V for the 8 heads is one contiguous 32 KB run of the pool.
-//   S^T (16 keys x 16 queries) = K Q^T    v_mfma_f32_16x16x32_bf16, K from LDS
-//   O^T (16 dims x 16 queries) += V^T P^T v_mfma_f32_16x16x16_bf16, V^T through
-//                                          ds_read_b64_tr_b16
-// After QK^T lane l holds query l%16 and keys 4*(l/16) + {0..3}, which is exactly
-// the B operand of the PV step, so probabilities never leave their lanes; row
-// statistics need two exchanges (lanes l^16 and l^32).
+// one-query (decode) attention: helpers
 // ---------------------------------------------------------------------------------
-constexpr int kDecHeads = 8;     // KV heads (waves) per decode workgroup
-constexpr int kDecKeys = 16;     // keys per decode tile
+constexpr int kDecKeys = kDecTileKeys;
 
 __device__ __forceinline__ int dec_parts(const Group& x, int n_hg) { return x.n_split > 1 ? x.n_split * n_hg : 0; }
 
@@ -824,30 +812,130 @@ __device__ __forceinline__ float sum_xor16(float x) {
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// s_waitcnt on vector memory only: wait until at most N loads of this wave are
+// outstanding (they complete in issue order)
+template <int N>
+__device__ __forceinline__ void wait_vmem_n() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// A wave-uniform element read through the scalar unit (the value lands in an
+// SGPR and waits on the scalar counter, not on the vector-memory queue).
+typedef __attribute__((address_space(4))) const int32_t const_i32_t;
+__device__ __forceinline__ int32_t scalar_load(const int32_t* p, int i) { return ((const_i32_t*)p)[i]; }
+
+// Global -> LDS copies written as inline assembly (global_load_lds_dword[x4], LDS
+// base in M0): the compiler does not see their LDS writes, so it adds no
+// vector-memory waits of its own before later LDS reads -- which it would do for
+// every LDS read after the builtin form, draining the whole prefetch queue.  The
+// kernel itself waits for them (wait_vmem_n, then a barrier) before reading what
+// they wrote.  `lds_wave_base` is wave-uniform; lane i writes bytes
+// [size*i, size*(i+1)) after it.
+__device__ __forceinline__ uint32_t lds_offset(const void* p) {
+    return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(const lds_void_t*)p);
+}
+__device__ __forceinline__ void dma_lds16(const void* src, const void* lds_wave_base) {
+    asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(lds_offset(lds_wave_base)) : "memory");
+}
+__device__ __forceinline__ void dma_lds4(const void* src, const void* lds_wave_base) {
+    asm volatile("s_nop 0\n\tglobal_load_lds_dword %0, off" ::"v"(src), "{m0}"(lds_offset(lds_wave_base)) : "memory");
+}
+
+// Workgroup barrier that leaves the vector-memory queue alone (__syncthreads
+// would also drain every outstanding global->LDS load): this wave's LDS writes are
+// waited for, and the compiler may move no memory access across it.
+__device__ __forceinline__ void barrier_keep_vmem() {
+    __builtin_amdgcn_s_waitcnt((15) | (3 << 14) | (7 << 4));   // lgkmcnt(0)
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+template <int D>
+constexpr int dec_stages() {
+    // K + V of the workgroup's heads x 16 keys, plus the tile's cos/sin rows, per
+    // stage, within 144 KB of LDS
+    return 147456 / (2 * dec_heads(D) * kDecKeys * D * 2 + kDecKeys * D / 2 * 8) > 4
+               ? 4
+               : 147456 / (2 * dec_heads(D) * kDecKeys * D * 2 + kDecKeys * D / 2 * 8);
+}
+
+// One pipeline stage of the decode kernel in LDS.  Each stage is its own LDS
+// object (as is each stage's position slot) so that reading one stage does not
+// make the compiler wait for the global->LDS loads still filling another.
+template <int D, bool ROPE>
+struct DecStage {
+    uint16_t k[dec_heads(D) * kDecKeys * D];   // [head][key][D], chunks swizzled by key
+    uint16_t v[dec_heads(D) * kDecKeys * D];
+    uint2 tab[ROPE ? kDecKeys * D / 2 : 2];     // [key][pair] (c,-s | s,c), chunks swizzled by key
+};
+
+template <int I>
+struct Idx {
+    static constexpr int value = I;
+};
+
+// ---------------------------------------------------------------------------------
+// decode_bf16
+//
+// One query per (request, query head).  Workgroup = (request, key split, group of
+// HW KV heads); wave w owns KV head HW*hg + w and its G <= 16 query heads as the 16
+// columns of 16x16 MFMA tiles.  A tile is 16 keys = one cache block, so its K or V
+// for the group's heads is one contiguous run of the pool.  Every global read of
+// the key loop goes straight to LDS (K unrotated, V, the cos/sin rows of the
+// tile's 16 keys, the positions of a later tile), NST tiles deep, so the only wait
+// per tile is for the oldest stage.  Each wave rotates its own K operand in
+// registers right before the MFMA: every K element is consumed by exactly one wave.
+//   S^T (16 keys x 16 queries) = K Q^T    v_mfma_f32_16x16x32_bf16
+//   O^T (16 dims x 16 queries) += V^T P^T v_mfma_f32_16x16x16_bf16, V^T through
+//                                          ds_read_b64_tr_b16
+// After QK^T lane l holds query l%16 and keys 4*(l/16) + {0..3}, which is exactly
+// the B operand of the PV step, so probabilities never leave their lanes; row
+// statistics need two exchanges (lanes l^16 and l^32).
+// ---------------------------------------------------------------------------------
 template <int D, int STYLE, bool ROPE, bool TABLE>
-__global__ void __launch_bounds__(kDecHeads * 64, 1) decode_bf16(const Plan plan, const Args a) {
+__global__ void __launch_bounds__(dec_heads(D) * 64, 1) decode_bf16(const Plan plan, const Args a) {
     typedef float f32x4_t __attribute__((ext_vector_type(4)));
     typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
-    constexpr int KD = D / 32;            // 16x16x32 contraction steps of QK^T
-    constexpr int DB = D / 16;            // 16-dim blocks of O^T
-    constexpr int CH = D / 8;             // 16-byte chunks per row
+    constexpr int KD = D / 32;             // 16x16x32 contraction steps of QK^T
+    constexpr int DB = D / 16;             // 16-dim blocks of O^T
+    constexpr int CH = D / 8;              // 16-byte chunks per K/V row
     constexpr int HALF = D / 2;
     constexpr int TK = kDecKeys;
-    constexpr int HW = kDecHeads;
-    constexpr int NT = HW * 64;           // threads
-    constexpr int TPK = D / 16;           // staging threads per (head, key)
-    constexpr int SU = HW * TK * TPK / NT; // staged (head, key) slices per thread
-    constexpr int HSZ = TK * D;           // elements of one head's tile
-    constexpr int DPL = HW * HSZ / 8 / NT; // direct 16-byte loads per lane per tile
-    static_assert(SU >= 1 && DPL >= 1, "decode tile shape");
+    constexpr int HW = dec_heads(D);
+    constexpr int NT = HW * 64;            // threads
+    constexpr int HSZ = TK * D;            // elements of one head's tile
+    constexpr int DPL = HW * HSZ / 8 / NT; // 16-byte direct loads per lane per tile, each of K and V
+    constexpr int TCH = TK * HALF / 2;     // 16-byte chunks (2 entries) of the tile's cos/sin rows
+    constexpr int TROW = HALF / 2;         // chunks per cos/sin row
+    constexpr int NST = dec_stages<D>();   // pipeline stages (tiles resident in LDS)
+    constexpr int LPS = 2 * DPL;           // unconditional loads per lane per stage
+    static_assert(DPL >= 1 && TROW >= 16 && NST >= 2 && NST <= 4, "decode tile shape");
+    static_assert((NST - 2) * LPS < 64, "vmcnt range");
+    typedef DecStage<D, ROPE> Stage;
 
-    __shared__ __attribute__((aligned(16))) uint16_t ks[2][HW * HSZ];
-    __shared__ __attribute__((aligned(16))) uint16_t vs[2][HW * HSZ];
+    __shared__ __attribute__((aligned(16))) Stage st0, st1, st2, st3;
+    __shared__ int32_t pos0[TK], pos1[TK], pos2[TK], pos3[TK];
     __shared__ uint64_t fstep[HALF];
+    auto stage = [&](auto b) -> Stage& {
+        constexpr int B = decltype(b)::value % NST;
+        if constexpr (B == 0) return st0;
+        else if constexpr (B == 1) return st1;
+        else if constexpr (B == 2) return st2;
+        else return st3;
+    };
+    auto pslot = [&](auto b) -> int32_t* {
+        constexpr int B = decltype(b)::value % NST;
+        if constexpr (B == 0) return pos0;
+        else if constexpr (B == 1) return pos1;
+        else if constexpr (B == 2) return pos2;
+        else return pos3;
+    };
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int c16 = lane & 15, q4 = lane >> 4;   // MFMA column (query) and row group
+    const int c16 = lane & 15, q4 = lane >> 4;   // MFMA column (query / key row) and row group
     const int n_hg = (a.hkv + HW - 1) / HW;
     int part_base;
     const Group g = plan.g[find_dec_group(plan, blockIdx.x, n_hg, part_base)];
@@ -863,9 +951,8 @@ __global__ void __launch_bounds__(kDecHeads * 64, 1) decode_bf16(const Plan plan
     const bool head_live = kvh < a.hkv;
     const int n_heads_here = min(HW, a.hkv - hg * HW);
 
-    if (ROPE && !TABLE)
+    if (ROPE)
         for (int i = tid; i < HALF; i += NT) fstep[i] = a.fstep[i];
-    const uint64_t* fsteps = TABLE ? a.fstep : fstep;
 
     const int32_t* btab = a.block_tables + (size_t)g.req * a.max_blocks;
     const uint16_t* kpool = static_cast<const uint16_t*>(a.k_pool);
@@ -873,24 +960,21 @@ __global__ void __launch_bounds__(kDecHeads * 64, 1) decode_bf16(const Plan plan
     const int kt0 = kv_lo & ~(TK - 1);
     const int n_tiles = (kv_hi - kt0 + TK - 1) / TK;
 
-    // ---- staging roles: slice sc of key kk of head hh (u-th unit of the thread)
-    auto unit = [&](int u, int& hh, int& kk, int& sc) {
-        const int x = tid + u * NT;
-        hh = x / (TK * TPK);
-        kk = (x / TPK) % TK;
-        sc = x % TPK;
-    };
-    struct Regs {
-        u32x4_t k[SU][2];
-        float4 cs[SU][4];
-        int32_t pos[SU];
-    };
-    int32_t next_pos[SU];  // positions of the staged keys, read one tile ahead
-    Regs regs;
-
     // keys outside [kv_lo, kv_hi) are loaded from the tile's first visible key, so
     // that nothing outside the window is read (their scores are masked)
     auto clamp_key = [&](int kt, int j) { return (j >= kv_lo && j < kv_hi) ? j : max(kt, kv_lo); };
+
+    // positions of tile u's 16 keys into position slot B (16 lanes of wave 0)
+    auto load_positions = [&](auto b, int u) {
+        if (!ROPE || wave != 0 || u >= n_tiles) return;
+        if (lane < TK) {
+            const int kt = kt0 + u * TK;
+            dma_lds4(a.positions + g.pos_off + clamp_key(kt, kt + lane), pslot(b));
+        }
+    };
+    load_positions(Idx<0>{}, 0);
+    if constexpr (NST > 2) load_positions(Idx<1>{}, 1);
+    if constexpr (NST > 3) load_positions(Idx<2>{}, 2);
 
     // ---- queries: B operand of S^T = K Q^T, rotated at the last token's position
     bf16x8_t qb[KD];
@@ -909,13 +993,14 @@ __global__ void __launch_bounds__(kDecHeads * 64, 1) decode_bf16(const Plan plan
             }
         }
         if (ROPE) {
-            if (!TABLE) __syncthreads();   // phase steps in LDS
             const int32_t pos = a.positions[g.pos_off + g.tok0];
+            const uint64_t* fs = TABLE ? a.fstep : fstep;
+            if (!TABLE) __syncthreads();   // phase steps in LDS
             if (STYLE == kNeox) {
 #pragma unroll
                 for (int kd = 0; kd < KD / 2; ++kd) {
                     float c[8], sn[8];
-                    rope_cs_n<8, TABLE>(a.rope_table, a.rope_len, HALF, fsteps, pos, kd * 32 + 8 * q4, c, sn);
+                    rope_cs_n<8, TABLE>(a.rope_table, a.rope_len, HALF, fs, pos, kd * 32 + 8 * q4, c, sn);
 #pragma unroll
                     for (int e = 0; e < 8; ++e) {
                         const float x = xf[kd][e], y = xf[kd + KD / 2][e];
@@ -927,7 +1012,7 @@ __global__ void __launch_bounds__(kDecHeads * 64, 1) decode_bf16(const Plan plan
 #pragma unroll
                 for (int kd = 0; kd < KD; ++kd) {
                     float c[4], sn[4];
-                    rope_cs_n<4, TABLE>(a.rope_table, a.rope_len, HALF, fsteps, pos, kd * 16 + 4 * q4, c, sn);
+                    rope_cs_n<4, TABLE>(a.rope_table, a.rope_len, HALF, fs, pos, kd * 16 + 4 * q4, c, sn);
 #pragma unroll
                     for (int m = 0; m < 4; ++m) {
                         const float x = xf[kd][2 * m], y = xf[kd][2 * m + 1];
@@ -946,106 +1031,56 @@ __global__ void __launch_bounds__(kDecHeads * 64, 1) decode_bf16(const Plan plan
             qb[kd] = __builtin_bit_cast(bf16x8_t, w);
         }
     }
+    wait_vmem();       // the first positions have landed
+    __syncthreads();   // ... for every wave; phase steps staged
 
-    // ---- loads of one tile: positions one tile ahead, K slices into registers
-    // (rotated on their way to LDS), V straight into LDS
-    auto load_pos = [&](int t) {
-        if (!ROPE) return;
+    // ---- tile u into stage B = u % NST, all straight into LDS.  Lane `lane` of
+    // wave `wave` fills 16-byte chunk p = (i*HW + wave)*64 + lane of the stage's K
+    // and V: head p / (HSZ/8), key row, physical chunk pc holding logical chunk
+    // pc ^ swz(key).  Chunk c < TCH of the tile's cos/sin rows (key c / TROW,
+    // physical chunk pc holding logical chunk pc ^ key: conflict-free reads across
+    // 16 keys) comes from the table, or is computed for positions outside it.  The
+    // positions of tile u + NST - 1 (the next tile issued after this one) go out
+    // first, into the slot tile u - 1 has finished with.
+    auto issue_tile = [&](auto b, int u) {
+        constexpr int B = decltype(b)::value % NST;
+        Stage& sg = stage(b);
+        const int kt = kt0 + u * TK;
+        load_positions(Idx<B + NST - 1>{}, u + NST - 1);
+        if (ROPE) {
+            const int32_t* pp = pslot(b);
 #pragma unroll
-        for (int u = 0; u < SU; ++u) {
-            int hh, kk, sc;
-            unit(u, hh, kk, sc);
-            const int j = kt0 + t * TK + kk;
-            next_pos[u] = (ROPE && t < n_tiles && j < kv_hi && j >= kv_lo) ? a.positions[g.pos_off + j] : 0;
-        }
-    };
-    auto issue_tile = [&](int t, int buf) {
-        const int kt = kt0 + t * TK;
-        const int blk = btab[kt >> 4];   // the tile is exactly one block
-#pragma unroll
-        for (int u = 0; u < SU && ROPE; ++u) {
-            int hh, kk, sc;
-            unit(u, hh, kk, sc);
-            const int j = clamp_key(kt, kt + kk);
-            const int hs = min(hh, n_heads_here - 1);   // heads past Hkv load a real head, never read
-            const uint16_t* kp = kpool + (((size_t)blk * a.hkv + hg * HW + hs) * kBlock + (j & 15)) * D;
-            regs.pos[u] = next_pos[u];
-            if (STYLE == kNeox) {
-                regs.k[u][0] = *reinterpret_cast<const u32x4_t*>(kp + sc * 8);
-                regs.k[u][1] = *reinterpret_cast<const u32x4_t*>(kp + HALF + sc * 8);
-            } else {
-                regs.k[u][0] = *reinterpret_cast<const u32x4_t*>(kp + sc * 16);
-                regs.k[u][1] = *reinterpret_cast<const u32x4_t*>(kp + sc * 16 + 8);
-            }
-            if (ROPE && TABLE && (uint32_t)regs.pos[u] < (uint32_t)a.rope_len) {
-                const float4* tp =
-                    reinterpret_cast<const float4*>(a.rope_table + ((size_t)regs.pos[u] * HALF + sc * 8) * 2);
-#pragma unroll
-                for (int k = 0; k < 4; ++k) regs.cs[u][k] = tp[k];
-            }
-        }
-#pragma unroll
-        for (int i = 0; i < DPL; ++i) {
-            const int p = (i * HW + wave) * 64 + lane;   // 16-byte chunk of the V tile
-            const int hh = p / (HSZ / 8), q = p % (HSZ / 8);
-            const int kk = q / CH, pc = q % CH;
-            const int j = clamp_key(kt, kt + kk);
-            const int hs = min(hh, n_heads_here - 1);
-            const size_t off = (((size_t)blk * a.hkv + hg * HW + hs) * kBlock + (j & 15)) * D + ((pc ^ swz<D>(kk)) << 3);
-            global_to_lds16(vpool + off, &vs[buf][(i * HW + wave) * 64 * 8]);
-            if (!ROPE) global_to_lds16(kpool + off, &ks[buf][(i * HW + wave) * 64 * 8]);
-        }
-    };
-    auto store_k = [&](int t, int buf) {
-        if (!ROPE) return;   // pre-rotated K went straight to LDS
-        const int kt = kt0 + t * TK;
-#pragma unroll
-        for (int u = 0; u < SU; ++u) {
-            int hh, kk, sc;
-            unit(u, hh, kk, sc);
-            const int j = kt + kk;
-            const bool ok = j >= kv_lo && j < kv_hi;
-            u32x4_t k0 = regs.k[u][0], k1 = regs.k[u][1];
-            if (ROPE) {
-                uint2 e[8];
-#pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    e[2 * k] = make_uint2(__float_as_uint(regs.cs[u][k].x), __float_as_uint(regs.cs[u][k].y));
-                    e[2 * k + 1] = make_uint2(__float_as_uint(regs.cs[u][k].z), __float_as_uint(regs.cs[u][k].w));
-                }
-                const bool need_cs = ok && !(TABLE && (uint32_t)regs.pos[u] < (uint32_t)a.rope_len);
-                if (!TABLE || __builtin_amdgcn_ballot_w64(need_cs) != 0) {
-                    if (need_cs) {
-#pragma unroll
-                        for (int k = 0; k < 8; ++k) {
-                            float c, sn;
-                            rope_cs(regs.pos[u], fsteps[sc * 8 + k], c, sn);
-                            e[k] = bf16_entry(c, sn);
+            for (int k = 0; k * NT < TCH; ++k) {
+                const int c = k * NT + tid;
+                if (c < TCH) {
+                    const int tkey = c / TROW, lc = (c % TROW) ^ tkey;
+                    const int32_t pos = pp[tkey];
+                    const bool in_table = TABLE && (uint32_t)pos < (uint32_t)a.rope_len;
+                    if (in_table)
+                        dma_lds16(a.rope_table + ((size_t)pos * HALF + 2 * lc) * 2, &sg.tab[(k * NT + wave * 64) * 2]);
+                    if (!TABLE || __builtin_amdgcn_ballot_w64(!in_table) != 0) {
+                        if (!in_table) {
+                            float c0, s0, c1, s1;
+                            rope_cs(pos, fstep[2 * lc], c0, s0);
+                            rope_cs(pos, fstep[2 * lc + 1], c1, s1);
+                            const uint2 e0 = bf16_entry(c0, s0), e1 = bf16_entry(c1, s1);
+                            *reinterpret_cast<u32x4_t*>(&sg.tab[c * 2]) = u32x4_t{e0.x, e0.y, e1.x, e1.y};
                         }
                     }
                 }
-                if (STYLE == kNeox) {
-#pragma unroll
-                    for (int m = 0; m < 4; ++m) {
-                        const uint32_t A = k0[m], B = k1[m];
-                        const uint32_t p0 = (A & 0xffffu) | (B << 16), p1 = (A >> 16) | (B & 0xffff0000u);
-                        k0[m] = pack_bf16(dot2_bf16(p0, e[2 * m].x), dot2_bf16(p1, e[2 * m + 1].x));
-                        k1[m] = pack_bf16(dot2_bf16(p0, e[2 * m].y), dot2_bf16(p1, e[2 * m + 1].y));
-                    }
-                } else {
-#pragma unroll
-                    for (int m = 0; m < 4; ++m) {
-                        k0[m] = pack_bf16(dot2_bf16(k0[m], e[m].x), dot2_bf16(k0[m], e[m].y));
-                        k1[m] = pack_bf16(dot2_bf16(k1[m], e[4 + m].x), dot2_bf16(k1[m], e[4 + m].y));
-                    }
-                }
             }
-            if (!ok) k0 = k1 = u32x4_t{0, 0, 0, 0};
-            uint16_t* row = &ks[buf][hh * HSZ + kk * D];
-            const int sw = swz<D>(kk);
-            const int ca = STYLE == kNeox ? sc : 2 * sc, cb = STYLE == kNeox ? sc + CH / 2 : 2 * sc + 1;
-            *reinterpret_cast<u32x4_t*>(row + ((ca ^ sw) << 3)) = k0;
-            *reinterpret_cast<u32x4_t*>(row + ((cb ^ sw) << 3)) = k1;
+        }
+        const int blk = scalar_load(btab, kt >> 4);   // the tile is exactly one block
+#pragma unroll
+        for (int i = 0; i < DPL; ++i) {
+            const int p = (i * HW + wave) * 64 + lane;
+            const int hh = p / (HSZ / 8), q = p % (HSZ / 8);
+            const int kk = q / CH, pc = q % CH;
+            const int j = clamp_key(kt, kt + kk);
+            const int hs = min(hh, n_heads_here - 1);   // heads past Hkv load a real head, never read
+            const size_t off = (((size_t)blk * a.hkv + hg * HW + hs) * kBlock + (j & 15)) * D + ((pc ^ swz<D>(kk)) << 3);
+            dma_lds16(kpool + off, &sg.k[(i * HW + wave) * 64 * 8]);
+            dma_lds16(vpool + off, &sg.v[(i * HW + wave) * 64 * 8]);
         }
     };
 
@@ -1054,78 +1089,129 @@ __global__ void __launch_bounds__(kDecHeads * 64, 1) decode_bf16(const Plan plan
     for (int db = 0; db < DB; ++db) acc[db] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     float m_run = kNegBig, l_run = 0.f;
 
-    // per-lane LDS offsets within one head's tile
+    // per-lane LDS offsets within one head's tile: K operand rows (key c16, logical
+    // chunk 4*kd + q4), the cos/sin chunks of the pairs those dims belong to (NeoX:
+    // pairs 32*kd + 8*q4 + e, kd < KD/2, 4 chunks each; GPT-J: pairs 16*kd + 4*q4 + e,
+    // 2 chunks each), and the transposing V reads (key 4*q4 + (lane%16)/4, dims
+    // 16*db + 4*(lane%4))
     int k_off[KD];
 #pragma unroll
-    for (int kd = 0; kd < KD; ++kd) k_off[kd] = c16 * D + (((kd * 4 + q4) ^ swz<D>(c16)) << 3);
+    for (int kd = 0; kd < KD; ++kd) k_off[kd] = wave * HSZ + c16 * D + (((kd * 4 + q4) ^ swz<D>(c16)) << 3);
+    constexpr int NTC = STYLE == kNeox ? 4 * (KD / 2) : 2 * KD;
+    int t_off[NTC];
+#pragma unroll
+    for (int u = 0; u < NTC; ++u) {
+        const int lc = STYLE == kNeox ? (u / 4) * 16 + 4 * q4 + (u % 4) : (u / 2) * 8 + 2 * q4 + (u % 2);
+        t_off[u] = c16 * HALF + 2 * (lc ^ c16);
+    }
     int v_off[DB];
     {
         const int key = 4 * q4 + ((lane & 15) >> 2);
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
             const int d = db * 16 + 4 * (lane & 3);
-            v_off[db] = key * D + (((d >> 3) ^ swz<D>(key)) << 3) + (d & 7);
+            v_off[db] = wave * HSZ + key * D + (((d >> 3) ^ swz<D>(key)) << 3) + (d & 7);
         }
     }
 
-    load_pos(0);
-    issue_tile(0, 0);
-    load_pos(1);
-    store_k(0, 0);
-    wait_vmem();
-    __syncthreads();
-
-    for (int t = 0; t < n_tiles; ++t) {
-        const int buf = t & 1;
+    // ---- one tile of the key loop, stage B = t % NST
+    auto step = [&](auto b, int t) {
+        Stage& sg = stage(b);
         const int kt = kt0 + t * TK;
-        const bool more = t + 1 < n_tiles;
-        if (more) {
-            issue_tile(t + 1, buf ^ 1);
-            load_pos(t + 2);
+        // tile t has landed once no more than the later issued stages' loads are
+        // outstanding; the barrier then also frees the stage read at t - 1
+        if (t + NST - 2 < n_tiles) wait_vmem_n<(NST - 2) * LPS>();
+        else wait_vmem();
+        barrier_keep_vmem();
+        if (t + NST - 1 < n_tiles) issue_tile(Idx<decltype(b)::value + NST - 1>{}, t + NST - 1);
+        if (!head_live) return;
+        lds_u16_t* vb = as_lds(sg.v);
+        u32x4_t kf[KD];
+#pragma unroll
+        for (int kd = 0; kd < KD; ++kd) kf[kd] = *reinterpret_cast<const u32x4_t*>(sg.k + k_off[kd]);
+        if (ROPE) {
+            // rotate the K operand in registers with entries (c,-s | s,c)
+            u32x4_t te[NTC];
+#pragma unroll
+            for (int u = 0; u < NTC; ++u) te[u] = *reinterpret_cast<const u32x4_t*>(&sg.tab[t_off[u]]);
+            if (STYLE == kNeox) {
+#pragma unroll
+                for (int kd = 0; kd < KD / 2; ++kd)
+#pragma unroll
+                    for (int m = 0; m < 4; ++m) {
+                        const uint32_t A = kf[kd][m], B = kf[kd + KD / 2][m];
+                        const uint32_t p0 = (A & 0xffffu) | (B << 16), p1 = (A >> 16) | (B & 0xffff0000u);
+                        const u32x4_t e = te[kd * 4 + m];   // pairs 2m, 2m+1 of this 8-dim run
+                        kf[kd][m] = pack_bf16(dot2_bf16(p0, e[0]), dot2_bf16(p1, e[2]));
+                        kf[kd + KD / 2][m] = pack_bf16(dot2_bf16(p0, e[1]), dot2_bf16(p1, e[3]));
+                    }
+            } else {
+#pragma unroll
+                for (int kd = 0; kd < KD; ++kd)
+#pragma unroll
+                    for (int m = 0; m < 4; ++m) {
+                        const u32x4_t e = te[kd * 2 + m / 2];
+                        const uint32_t ex = e[2 * (m & 1)], ey = e[2 * (m & 1) + 1];
+                        kf[kd][m] = pack_bf16(dot2_bf16(kf[kd][m], ex), dot2_bf16(kf[kd][m], ey));
+                    }
+            }
         }
-        if (head_live) {
-            const uint16_t* kb = &ks[buf][wave * HSZ];
-            lds_u16_t* vb = as_lds(&vs[buf][wave * HSZ]);
-            f32x4_t sc4 = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        f32x4_t sc4 = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int kd = 0; kd < KD; ++kd) {
-                const bf16x8_t af = *reinterpret_cast<const bf16x8_t*>(kb + k_off[kd]);
-                sc4 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, qb[kd], sc4, 0, 0, 0);
-            }
-            if (kt < kv_lo || kt + TK > kv_hi) {
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int key = kt + 4 * q4 + r;
-                    if (key < kv_lo || key >= kv_hi) sc4[r] = -INFINITY;
-                }
-            }
-            float mx = fmaxf(fmaxf(sc4[0], sc4[1]), fmaxf(sc4[2], sc4[3]));
-            mx = max_xor32(max_xor16(mx));
-            if (__builtin_amdgcn_ballot_w64(mx > m_run + 8.f) != 0) {
-                const float m_new = fmaxf(m_run, mx);
-                const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-                l_run *= alpha;
-#pragma unroll
-                for (int db = 0; db < DB; ++db) acc[db] *= alpha;
-                m_run = m_new;
-            }
-            float p[4];
+        for (int kd = 0; kd < KD; ++kd)
+            sc4 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kf[kd]), qb[kd], sc4, 0, 0, 0);
+        if (kt < kv_lo || kt + TK > kv_hi) {
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                p[r] = __builtin_amdgcn_exp2f(sc4[r] - m_run);
-                l_run += p[r];
-            }
-            const uint32_t pw[2] = {pack_bf16(p[0], p[1]), pack_bf16(p[2], p[3])};
-            const bf16x4_t pb = __builtin_bit_cast(bf16x4_t, pw);
-#pragma unroll
-            for (int db = 0; db < DB; ++db) {
-                const bf16x4_t af = __builtin_bit_cast(bf16x4_t, lds_read_tr(vb + v_off[db]));
-                acc[db] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(af, pb, acc[db], 0, 0, 0);
+                const int key = kt + 4 * q4 + r;
+                if (key < kv_lo || key >= kv_hi) sc4[r] = -INFINITY;
             }
         }
-        if (more) store_k(t + 1, buf ^ 1);
-        wait_vmem();
-        __syncthreads();
+        float mx = fmaxf(fmaxf(sc4[0], sc4[1]), fmaxf(sc4[2], sc4[3]));
+        mx = max_xor32(max_xor16(mx));
+        if (__builtin_amdgcn_ballot_w64(mx > m_run + 8.f) != 0) {
+            const float m_new = fmaxf(m_run, mx);
+            const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+            l_run *= alpha;
+#pragma unroll
+            for (int db = 0; db < DB; ++db) acc[db] *= alpha;
+            m_run = m_new;
+        }
+        float p[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            p[r] = __builtin_amdgcn_exp2f(sc4[r] - m_run);
+            l_run += p[r];
+        }
+        const uint32_t pw[2] = {pack_bf16(p[0], p[1]), pack_bf16(p[2], p[3])};
+        const bf16x4_t pb = __builtin_bit_cast(bf16x4_t, pw);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+            const bf16x4_t af = __builtin_bit_cast(bf16x4_t, lds_read_tr(vb + v_off[db]));
+            acc[db] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(af, pb, acc[db], 0, 0, 0);
+        }
+    };
+
+    // prologue: stages 0 .. NST-2 in flight (each issue reuses the position slot
+    // the previous one read, hence the barriers)
+    issue_tile(Idx<0>{}, 0);
+    if constexpr (NST > 2) {
+        barrier_keep_vmem();
+        if (1 < n_tiles) issue_tile(Idx<1>{}, 1);
+    }
+    if constexpr (NST > 3) {
+        barrier_keep_vmem();
+        if (2 < n_tiles) issue_tile(Idx<2>{}, 2);
+    }
+    for (int t = 0; t < n_tiles; t += NST) {
+        step(Idx<0>{}, t);
+        if (t + 1 < n_tiles) step(Idx<1>{}, t + 1);
+        if constexpr (NST > 2) {
+            if (t + 2 < n_tiles) step(Idx<2>{}, t + 2);
+        }
+        if constexpr (NST > 3) {
+            if (t + 3 < n_tiles) step(Idx<3>{}, t + 3);
+        }
     }
 
     // ---- epilogue: lane l holds query column l%16 and dims 16*db + 4*(l/16) + r
@@ -1156,7 +1242,8 @@ __global__ void __launch_bounds__(kDecHeads * 64, 1) decode_bf16(const Plan plan
 template <int D>
 __global__ void __launch_bounds__(kMergeRows * D / 4) decode_merge(const Plan plan, const Args a) {
     constexpr int TPR = D / 4;
-    const int n_hg = (a.hkv + kDecHeads - 1) / kDecHeads;
+    constexpr int HW = dec_heads(D);
+    const int n_hg = (a.hkv + HW - 1) / HW;
     const int per_req = (a.hq + kMergeRows - 1) / kMergeRows;
     // locate the request among the split groups
     int part = plan.part0, merge = 0, gi = -1;
@@ -1175,7 +1262,7 @@ __global__ void __launch_bounds__(kMergeRows * D / 4) decode_merge(const Plan pl
     const int q4 = (int)threadIdx.x % TPR;
     if (qh >= a.hq) return;
     const int kvh = qh / a.group, c = qh - kvh * a.group;
-    const int hg = kvh / kDecHeads, prow = (kvh % kDecHeads) * 16 + c;
+    const int hg = kvh / HW, prow = (kvh % HW) * 16 + c;
     const int L = g.tok0 + 1;
     float M = kNegBig, den = 0.f;
     float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -1305,7 +1392,7 @@ hipError_t launch_attn_t(int dtype, const Plan& plan, const Args& a, hipStream_t
 
 template <int D, int STYLE, bool ROPE, bool TABLE>
 hipError_t launch_dec_t(const Plan& plan, const Args& a, hipStream_t st) {
-    hipLaunchKernelGGL((decode_bf16<D, STYLE, ROPE, TABLE>), dim3(plan.n_items), dim3(kDecHeads * 64), 0, st, plan, a);
+    hipLaunchKernelGGL((decode_bf16<D, STYLE, ROPE, TABLE>), dim3(plan.n_items), dim3(dec_heads(D) * 64), 0, st, plan, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (plan.n_merge > 0) {
