@@ -261,11 +261,33 @@ __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70)
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
-// 16 bytes per lane from global memory straight into LDS (no registers): the wave
-// writes 64 consecutive 16-byte chunks starting at `lds_dst` (wave-uniform).
-__device__ __forceinline__ void global_to_lds16(const uint16_t* src, uint16_t* lds_dst) {
-    __builtin_amdgcn_global_load_lds(src, (lds_void_t*)lds_dst, 16, 0, 0);
+// Global -> LDS copies written as inline assembly (global_load_lds_dword[x4], LDS
+// base in M0): the compiler does not see their LDS writes, so it adds no
+// vector-memory waits of its own before later LDS reads -- which it would do for
+// every LDS read after the builtin form, draining the whole prefetch queue.  The
+// kernel itself waits for them (wait_vmem_n, then a barrier) before reading what
+// they wrote.  `lds_wave_base` is wave-uniform; lane i writes bytes
+// [size*i, size*(i+1)) after it.
+__device__ __forceinline__ uint32_t lds_offset(const void* p) {
+    return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(const lds_void_t*)p);
 }
+__device__ __forceinline__ void dma_lds16(const void* src, const void* lds_wave_base) {
+    asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(lds_offset(lds_wave_base)) : "memory");
+}
+__device__ __forceinline__ void dma_lds4(const void* src, const void* lds_wave_base) {
+    asm volatile("s_nop 0\n\tglobal_load_lds_dword %0, off" ::"v"(src), "{m0}"(lds_offset(lds_wave_base)) : "memory");
+}
+
+// Workgroup barrier that leaves the vector-memory queue alone (__syncthreads
+// would also drain every outstanding global->LDS load): this wave's LDS writes are
+// waited for, and the compiler may move no memory access across it.
+__device__ __forceinline__ void barrier_keep_vmem() {
+    __builtin_amdgcn_s_waitcnt((15) | (3 << 14) | (7 << 4));   // lgkmcnt(0)
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
 
 // ---------------------------------------------------------------------------------
 // prefill_bf16
@@ -426,6 +448,7 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
     // `wave` fills 16-byte chunk p = (DPW*wave + i)*64 + lane of the tile, i.e. row
     // p / CH, physical chunk p % CH, which holds logical chunk (p % CH) ^ swz(row)
     constexpr int DPW = BN * CH / (64 * kWaves);
+    static_assert(kWaves >= 2, "metadata copies use two waves");
     const int wave_u = __builtin_amdgcn_readfirstlane(wave);
     auto dkey = [&](int i) { return ((DPW * wave_u + i) * 64 + lane) / CH; };
     auto dchunk = [&](int i) {
@@ -433,56 +456,49 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
         return (p % CH) ^ swz<D>(p / CH);
     };
 
-    // per-key metadata one tile ahead of the data loads: the block and position of
-    // the stager's key, and for every direct-load lane the slot (block*16 + offset)
-    // of its key -- or, for keys outside [kv_lo, kv_hi), of the tile's first visible
-    // key, so that no key outside the window is ever read (its score is masked).
-    struct Meta {
-        int phys[SU];
-        int32_t pos[SU];
-        int dslot[DPW];
+    // per-key metadata two tiles ahead of its use, copied global->LDS with no
+    // register round trip (so no load waits on it): the positions of the tile's 64
+    // keys (wave 0) and its 4 block ids (wave 1), from keys clamped into the window
+    // -- a key outside [kv_lo, kv_hi) stands for the tile's first visible key, so
+    // that nothing outside the window is ever read (its score is masked).
+    __shared__ int32_t mpos[2][BN];
+    __shared__ int32_t mblk[2][BN / kBlock];
+    auto clamp_key = [&](int kt, int j) { return (j >= kv_lo && j < kv_hi) ? j : max(kt, kv_lo); };
+    auto dma_meta = [&](int t) {
+        if (t >= n_tiles) return;
+        const int kt = kt0 + t * BN;
+        if (ROPE && wave_u == 0) {
+            dma_lds4(a.positions + g.pos_off + clamp_key(kt, kt + lane), &mpos[t & 1][0]);
+        } else if (wave_u == 1 && lane < BN / kBlock) {
+            const int blk = min((kt >> 4) + lane, (kv_hi - 1) >> 4);
+            dma_lds4(btab + blk, &mblk[t & 1][0]);
+        }
     };
-    auto load_meta = [&](int t, Meta& m) {
+    auto issue_direct = [&](int t, int buf) {
         const int kt = kt0 + t * BN;
 #pragma unroll
-        for (int u = 0; u < SU; ++u) m.phys[u] = m.pos[u] = 0;
-        if (t >= n_tiles) return;
-#pragma unroll
-        for (int u = 0; u < SU; ++u) {
-            const int j = kt + kk + u * KSTEP;
-            if (stager && j >= kv_lo && j < kv_hi) {
-                m.phys[u] = btab[j >> 4];
-                m.pos[u] = a.positions[g.pos_off + j];
-            }
-        }
-        const int j_ok = max(kt, kv_lo);
-#pragma unroll
         for (int i = 0; i < DPW; ++i) {
-            const int jd = kt + dkey(i);
-            const int jj = (jd >= kv_lo && jd < kv_hi) ? jd : j_ok;
-            m.dslot[i] = btab[jj >> 4] * kBlock + (jj & 15);
-        }
-    };
-    auto issue_direct = [&](int buf, const Meta& m) {
-#pragma unroll
-        for (int i = 0; i < DPW; ++i) {
-            const size_t row_off = (((size_t)(m.dslot[i] >> 4) * a.hkv + kvh) * kBlock + (m.dslot[i] & 15)) * D;
+            const int jj = clamp_key(kt, kt + dkey(i));
+            const int phys = mblk[t & 1][(jj - kt) >> 4];
+            const size_t row_off = (((size_t)phys * a.hkv + kvh) * kBlock + (jj & 15)) * D;
             const int lds_off = (DPW * wave_u + i) * 64 * 8;
-            global_to_lds16(vpool + row_off + dchunk(i) * 8, &vs[buf][lds_off]);
-            if (!ROPE) global_to_lds16(kpool + row_off + dchunk(i) * 8, &ks[buf][lds_off]);
+            dma_lds16(vpool + row_off + dchunk(i) * 8, &vs[buf][lds_off]);
+            if (!ROPE) dma_lds16(kpool + row_off + dchunk(i) * 8, &ks[buf][lds_off]);
         }
     };
-    auto load_tile = [&](int t, const Meta& m, TileRegs* rr) {
+    auto load_tile = [&](int t, TileRegs* rr) {
         if (!stager) return;
 #pragma unroll
         for (int u = 0; u < SU; ++u) {
         TileRegs& r = rr[u];
-        const int j = kt0 + t * BN + kk + u * KSTEP;
+        const int kr = kk + u * KSTEP;
+        const int j = kt0 + t * BN + kr;
         r.ok = j >= kv_lo && j < kv_hi;
-        r.pos = m.pos[u];
+        r.pos = mpos[t & 1][kr];
         r.k[0] = r.k[1] = u32x4_t{0, 0, 0, 0};
         if (r.ok) {
-            const uint16_t* kp = kpool + (((size_t)m.phys[u] * a.hkv + kvh) * kBlock + (j & 15)) * D;
+            const int phys = mblk[t & 1][kr >> 4];
+            const uint16_t* kp = kpool + (((size_t)phys * a.hkv + kvh) * kBlock + (j & 15)) * D;
             if (STYLE == kNeox) {
                 r.k[0] = *reinterpret_cast<const u32x4_t*>(kp + sc * 8);
                 r.k[1] = *reinterpret_cast<const u32x4_t*>(kp + HALF + sc * 8);
@@ -561,13 +577,13 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
     // ---- prologue: the queries' loads and the first tile's loads are all in flight
     // before the first wait
     TileRegs regs[SU];
-    Meta meta_n, meta_nn;
     q_issue();
-    load_meta(0, meta_n);
-    issue_direct(0, meta_n);
-    load_tile(0, meta_n, regs);
-    load_meta(1, meta_nn);
-    if (ROPE && !TABLE) __syncthreads();   // phase steps ready
+    dma_meta(0);
+    dma_meta(1);
+    wait_vmem();
+    __syncthreads();   // metadata of tiles 0 and 1 landed; phase steps staged
+    issue_direct(0, 0);
+    load_tile(0, regs);
     q_finish();
     store_tile(0, regs);
     wait_vmem();
@@ -601,7 +617,8 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
         const bool more = t + 1 < n_tiles;
         // direct loads of the next tile (no registers) go out first; the rotated-K
         // register loads wait until the score tile is dead (after the softmax)
-        if (more) issue_direct(buf ^ 1, meta_nn);
+        dma_meta(t + 2);   // into the slot tile t's metadata has left
+        if (more) issue_direct(t + 1, buf ^ 1);
         if (wave_live) {
             const uint16_t* kb = &ks[buf][0];
             lds_u16_t* vb = as_lds(&vs[buf][0]);
@@ -660,7 +677,7 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
                     }
                     pb[k2] = __builtin_bit_cast(bf16x8_t, w);
                 }
-                if (mb == NH - 1 && more) load_tile(t + 1, meta_nn, regs);
+                if (mb == NH - 1 && more) load_tile(t + 1, regs);
                 // ---- O^T += V^T P^T
 #pragma unroll
                 for (int db = 0; db < DB; ++db)
@@ -675,8 +692,7 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
             }
         }
         if (more) {
-            if (!wave_live) load_tile(t + 1, meta_nn, regs);
-            load_meta(t + 2, meta_nn);
+            if (!wave_live) load_tile(t + 1, regs);
             store_tile(buf ^ 1, regs);
         }
         wait_vmem();
@@ -824,33 +840,6 @@ __device__ __forceinline__ void wait_vmem_n() {
 // SGPR and waits on the scalar counter, not on the vector-memory queue).
 typedef __attribute__((address_space(4))) const int32_t const_i32_t;
 __device__ __forceinline__ int32_t scalar_load(const int32_t* p, int i) { return ((const_i32_t*)p)[i]; }
-
-// Global -> LDS copies written as inline assembly (global_load_lds_dword[x4], LDS
-// base in M0): the compiler does not see their LDS writes, so it adds no
-// vector-memory waits of its own before later LDS reads -- which it would do for
-// every LDS read after the builtin form, draining the whole prefetch queue.  The
-// kernel itself waits for them (wait_vmem_n, then a barrier) before reading what
-// they wrote.  `lds_wave_base` is wave-uniform; lane i writes bytes
-// [size*i, size*(i+1)) after it.
-__device__ __forceinline__ uint32_t lds_offset(const void* p) {
-    return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(const lds_void_t*)p);
-}
-__device__ __forceinline__ void dma_lds16(const void* src, const void* lds_wave_base) {
-    asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(lds_offset(lds_wave_base)) : "memory");
-}
-__device__ __forceinline__ void dma_lds4(const void* src, const void* lds_wave_base) {
-    asm volatile("s_nop 0\n\tglobal_load_lds_dword %0, off" ::"v"(src), "{m0}"(lds_offset(lds_wave_base)) : "memory");
-}
-
-// Workgroup barrier that leaves the vector-memory queue alone (__syncthreads
-// would also drain every outstanding global->LDS load): this wave's LDS writes are
-// waited for, and the compiler may move no memory access across it.
-__device__ __forceinline__ void barrier_keep_vmem() {
-    __builtin_amdgcn_s_waitcnt((15) | (3 << 14) | (7 << 4));   // lgkmcnt(0)
-    __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    __builtin_amdgcn_s_barrier();
-    __atomic_signal_fence(__ATOMIC_SEQ_CST);
-}
 
 template <int D>
 constexpr int dec_stages() {
