@@ -230,6 +230,8 @@ void make_launches(const pic_config* c, HostPlan& hp, std::vector<pic::Plan>& la
             const int64_t n_pad = hp.dec_kernel ? n : round_up(n, 8);
             if (item + n_pad > INT32_MAX / 2 && p.n_groups > 0) break;
             g.item_base = (int32_t)item;
+            g.part_base = (int32_t)part;
+            g.merge_base = (int32_t)merge;
             item += n_pad;
             if (hp.dec_kernel) {
                 if (g.n_split > 1) {
@@ -429,7 +431,6 @@ pic_status pic_plan_debug(const pic_config* cfg, const pic_batch_host* batch, in
         ++n;
     };
     for (const auto& p : launches) {
-        int64_t part_base = p.part0;
         for (int gi = 0; gi < p.n_groups; ++gi) {
             const pic::Group& g = p.g[gi];
             if (hp.dec_kernel) {
@@ -440,11 +441,10 @@ pic_status pic_plan_debug(const pic_config* cfg, const pic_batch_host* batch, in
                     if (kl >= kh) continue;
                     for (int kvh = 0; kvh < cfg->num_kv_heads; ++kvh) {
                         const int32_t slot =
-                            g.n_split > 1 ? (int32_t)(part_base + s * n_hg + kvh / pic::dec_heads(cfg->head_dim)) : -1;
+                            g.n_split > 1 ? (int32_t)(g.part_base + s * n_hg + kvh / pic::dec_heads(cfg->head_dim)) : -1;
                         emit(g.req, kvh, 0, G, kl, kh, g.tok0, slot);
                     }
                 }
-                if (g.n_split > 1) part_base += g.n_split * n_hg;
                 continue;
             }
             if (cfg->dtype == PIC_F32) {
@@ -465,10 +465,9 @@ pic_status pic_plan_debug(const pic_config* cfg, const pic_batch_host* batch, in
                         const int32_t kh = std::min(kl + g.split_keys, t_last + 1);
                         if (kl >= kh) continue;
                         const int32_t slot =
-                            g.n_split > 1 ? (int32_t)part_base + (kvh * g.n_split + s) * g.n_rt + rt : -1;
+                            g.n_split > 1 ? g.part_base + (kvh * g.n_split + s) * g.n_rt + rt : -1;
                         emit(g.req, kvh, rl, rh, kl, kh, g.tok0, slot);
                     }
-            if (g.n_split > 1) part_base += (int64_t)g.n_rt * cfg->num_kv_heads * g.n_split;
         }
     }
     *n_items = (int32_t)std::min<int64_t>(n, INT32_MAX);

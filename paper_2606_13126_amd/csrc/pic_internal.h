@@ -28,10 +28,12 @@ constexpr int kDecMaxG = 16;      // query heads per KV head the decode kernel h
 constexpr int dec_heads(int head_dim) { return head_dim == 128 ? PIC_DEC_HEADS_D128 : 8; }
 
 // One query span of one request (prefill) or one request's last token (decode).
-// Its work items are (row tile, KV head, key split) triples, enumerated from
-// item_base.  Partial results of split groups take consecutive slots in group
-// order from Plan::part0, and their merge blocks consecutive block indices; the
-// kernels recover both bases by summing over the preceding groups.
+// Its work items are (row tile, KV head, key split) triples -- (key split, head
+// group) for the decode kernel -- enumerated from item_base.  Partial results of
+// split groups take consecutive slots from part_base, and their merge blocks
+// consecutive block indices of the merge launch from merge_base.  item_base and
+// merge_base are non-decreasing over a launch's groups, so a block finds its group
+// by binary search.
 struct Group {
     int32_t req;         // request index (row of the block table)
     int32_t tok0;        // sequence index of the span's first query token
@@ -42,7 +44,9 @@ struct Group {
     int32_t n_rt;        // row tiles (ceil(n_tok * G / kTileRows))
     int32_t n_split;     // key splits per (row tile, KV head)
     int32_t split_keys;  // keys per split (a multiple of kTileKeys)
-    int32_t item_base;   // first item (block index) of the group; a multiple of 8
+    int32_t item_base;   // first item (block index) of the group; a multiple of 8 (prefill)
+    int32_t part_base;   // first partial slot (split groups)
+    int32_t merge_base;  // first block of the merge launch (split groups)
 };
 
 struct Plan {
@@ -52,6 +56,18 @@ struct Plan {
     int32_t part0;       // first partial slot of this launch's split groups
     Group g[kMaxGroups];
 };
+
+// last group whose `field` is <= b (the fields are non-decreasing over groups)
+template <int32_t Group::*field>
+__host__ __device__ inline int plan_search(const Plan& p, int b) {
+    int lo = 0, hi = p.n_groups - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (p.g[mid].*field <= b) lo = mid;
+        else hi = mid - 1;
+    }
+    return lo;
+}
 
 struct Args {
     // RoPE phase step of pair i as a 64-bit fraction of a revolution per position:

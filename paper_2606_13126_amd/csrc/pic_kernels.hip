@@ -172,40 +172,11 @@ __global__ void __launch_bounds__(256) rope_rotate_kernel(T* __restrict__ x, int
 }
 
 // Partial slots and merge blocks of a split group.
-__device__ __forceinline__ int group_parts(const Group& x, int hkv) {
-    return x.n_split > 1 ? x.n_rt * hkv * x.n_split : 0;
-}
-__device__ __forceinline__ int group_merges(const Group& x, int hkv) {
-    return x.n_split > 1 ? x.n_rt * hkv * (kTileRows / kMergeRows) : 0;
-}
-
-// Group of an attention block (groups are sorted by item_base) and its first
-// partial slot.
-__device__ __forceinline__ int find_group(const Plan& plan, int bid, int hkv, int& part_base) {
-    int gi = 0, part = plan.part0;
-    while (gi + 1 < plan.n_groups && plan.g[gi + 1].item_base <= bid) {
-        part += group_parts(plan.g[gi], hkv);
-        ++gi;
-    }
-    part_base = part;
+// Group of an attention block and its first partial slot.
+__device__ __forceinline__ int find_group(const Plan& plan, int bid, int& part_base) {
+    const int gi = plan_search<&Group::item_base>(plan, bid);
+    part_base = plan.g[gi].part_base;
     return gi;
-}
-
-// Group of a merge block, its first partial slot and its first merge block.
-__device__ __forceinline__ int find_merge_group(const Plan& plan, int bid, int hkv, int& part_base,
-                                                int& merge_base) {
-    int part = plan.part0, merge = 0;
-    for (int i = 0; i < plan.n_groups; ++i) {
-        const int nb = group_merges(plan.g[i], hkv);
-        if (bid < merge + nb) {
-            part_base = part;
-            merge_base = merge;
-            return i;
-        }
-        merge += nb;
-        part += group_parts(plan.g[i], hkv);
-    }
-    return -1;
 }
 
 constexpr int kWaves = kTileRows / 32;   // wave w owns rows [32w, 32w+32); 2 waves per SIMD
@@ -298,12 +269,13 @@ __device__ __forceinline__ void barrier_keep_vmem() {
 // while the current one is consumed):
 //   ks[64][D]  rotated K, bf16, 16-byte chunks XOR-swizzled by key;
 //   vs[64][D]  V as stored (bf16), same swizzle.
-//   S^T (64 keys x 32 queries) = K Q^T: A = K from LDS, B = Q in registers.  After
-//   the MFMA lane l holds query l%32 and keys 8*(j/4) + 4*(l/32) + j%4 (j = 0..15) of
-//   each 32-key half, so row statistics need one exchange with lane l^32.  Those 16
-//   probabilities, in that key order, are the B operand of O^T = V^T P^T for two
-//   16-key steps; the matching A operand (32 dims x the same 8 keys per lane) comes
-//   straight from the untransposed V tile through ds_read_b64_tr_b16.
+//   S^T (64 keys x 32 queries) = K Q^T: A = K from LDS, B = Q in registers, as two
+//   32-key halves whose MFMA chains interleave.  After the MFMA lane l holds query
+//   l%32 and keys 8*(j/4) + 4*(l/32) + j%4 (j = 0..15) of each half, so row
+//   statistics need one exchange with lane l^32, and one softmax decision covers the
+//   tile.  Those probabilities, in that key order, are the B operand of O^T = V^T P^T
+//   for 16-key steps; the matching A operand (32 dims x the same 8 keys per lane)
+//   comes straight from the untransposed V tile through ds_read_b64_tr_b16.
 // ---------------------------------------------------------------------------------
 template <int D, int STYLE, bool ROPE, bool TABLE>
 __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const Plan plan, const Args a) {
@@ -327,7 +299,7 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
 
     const int bid = blockIdx.x;
     int part_base;
-    const Group g = plan.g[find_group(plan, bid, a.hkv, part_base)];
+    const Group g = plan.g[find_group(plan, bid, part_base)];
     const int G = a.group;
     const int n_clusters = a.hkv * g.n_split;
     const int li = bid - g.item_base;
@@ -623,21 +595,23 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
             const uint16_t* kb = &ks[buf][0];
             lds_u16_t* vb = as_lds(&vs[buf][0]);
             const bool masked = kt < kv_lo || kt + BN > kv_hi || kt + BN - 1 > wave_tmin;
-            // the tile is consumed as two 32-key halves: S^T half -> mask -> softmax ->
-            // O^T += V^T P^T half; the second half's QK^T does not depend on the first
-            // half's softmax, which leaves MFMA work to overlap with VALU work
+            // ---- S^T (32 keys x 32 queries) = K Q^T for both halves of the tile, the two
+            // MFMA chains interleaved (each accumulator was last written two MFMAs back)
+            f32x16_t s[NH];
 #pragma unroll
-            for (int mb = 0; mb < NH; ++mb) {
-                // ---- S^T (32 keys x 32 queries) = K Q^T
-                f32x16_t s = f32x16_t{};
+            for (int mb = 0; mb < NH; ++mb) s[mb] = f32x16_t{};
 #pragma unroll
-                for (int kd = 0; kd < KD; ++kd) {
+            for (int kd = 0; kd < KD; ++kd)
+#pragma unroll
+                for (int mb = 0; mb < NH; ++mb) {
                     const bf16x8_t af = *reinterpret_cast<const bf16x8_t*>(kb + k_off[kd] + mb * 32 * D);
-                    s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, qb[kd], s, 0, 0, 0);
+                    s[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, qb[kd], s[mb], 0, 0, 0);
                 }
-                // ---- window mask on tiles that cross a boundary of the visible set: a
-                // bit mask of the visible keys relative to this lane's first key
-                if (masked) {
+            // ---- window mask on tiles that cross a boundary of the visible set: a bit
+            // mask of the visible keys relative to this lane's first key of each half
+            if (masked) {
+#pragma unroll
+                for (int mb = 0; mb < NH; ++mb) {
                     const int base = kt + mb * 32 + 4 * hi;
                     const int lo = max(kv_lo - base, 0), top = min(hi_key - base, 31);
                     const uint32_t upto = (2u << (uint32_t)max(top, 0)) - 1u;
@@ -645,51 +619,55 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
 #pragma unroll
                     for (int j = 0; j < 16; ++j) {
                         const int c = 8 * (j >> 2) + (j & 3);
-                        s[j] = (vis & (1u << c)) ? s[j] : -INFINITY;
+                        s[mb][j] = (vis & (1u << c)) ? s[mb][j] : -INFINITY;
                     }
                 }
-                // ---- online softmax in the log2 domain.  The reference maximum only
-                // moves when some row's maximum grows by more than 8 (probabilities stay
-                // below 2^8), so most halves skip rescaling the accumulators.
-                float mx = kNegBig;
+            }
+            // ---- online softmax in the log2 domain, one decision per tile.  The
+            // reference maximum only moves when some row's maximum grows by more than 8
+            // (probabilities stay below 2^8), so most tiles skip rescaling.
+            float mx = kNegBig;
 #pragma unroll
-                for (int j = 0; j < 16; ++j) mx = fmaxf(mx, s[j]);
-                mx = max_xor32(mx);
-                if (__builtin_amdgcn_ballot_w64(mx > m_run + 8.f) != 0) {
-                    const float m_new = fmaxf(m_run, mx);
-                    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-                    l_run *= alpha;
+            for (int mb = 0; mb < NH; ++mb)
 #pragma unroll
-                    for (int db = 0; db < DB; ++db) acc[db] *= alpha;
-                    m_run = m_new;
-                }
-                // probabilities: fp32 for the row sum, bf16 for P V
-                bf16x8_t pb[2];
+                for (int j = 0; j < 16; ++j) mx = fmaxf(mx, s[mb][j]);
+            mx = max_xor32(mx);
+            if (__builtin_amdgcn_ballot_w64(mx > m_run + 8.f) != 0) {
+                const float m_new = fmaxf(m_run, mx);
+                const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+                l_run *= alpha;
+#pragma unroll
+                for (int db = 0; db < DB; ++db) acc[db] *= alpha;
+                m_run = m_new;
+            }
+            // probabilities: fp32 for the row sum, bf16 for P V
+            bf16x8_t pb[2 * NH];
+#pragma unroll
+            for (int mb = 0; mb < NH; ++mb)
 #pragma unroll
                 for (int k2 = 0; k2 < 2; ++k2) {
                     u32x4_t w;
 #pragma unroll
                     for (int m = 0; m < 4; ++m) {
-                        const float p0 = __builtin_amdgcn_exp2f(s[8 * k2 + 2 * m] - m_run);
-                        const float p1 = __builtin_amdgcn_exp2f(s[8 * k2 + 2 * m + 1] - m_run);
+                        const float p0 = __builtin_amdgcn_exp2f(s[mb][8 * k2 + 2 * m] - m_run);
+                        const float p1 = __builtin_amdgcn_exp2f(s[mb][8 * k2 + 2 * m + 1] - m_run);
                         l_run += p0 + p1;
                         w[m] = pack_bf16(p0, p1);
                     }
-                    pb[k2] = __builtin_bit_cast(bf16x8_t, w);
+                    pb[2 * mb + k2] = __builtin_bit_cast(bf16x8_t, w);
                 }
-                if (mb == NH - 1 && more) load_tile(t + 1, regs);
-                // ---- O^T += V^T P^T
+            if (more) load_tile(t + 1, regs);
+            // ---- O^T += V^T P^T, 16 keys per step, the DB independent accumulators in turn
 #pragma unroll
-                for (int db = 0; db < DB; ++db)
+            for (int k4 = 0; k4 < 2 * NH; ++k4)
 #pragma unroll
-                    for (int k2 = 0; k2 < 2; ++k2) {
-                        const int row0 = (mb * 32 + 16 * k2) * D;
-                        const s16x4_t both[2] = {lds_read_tr(vb + v_off[db] + row0),
-                                                 lds_read_tr(vb + (v_off[db] ^ (kSwz8 << 3)) + 8 * D + row0)};
-                        const bf16x8_t af = __builtin_bit_cast(bf16x8_t, both);
-                        acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, pb[k2], acc[db], 0, 0, 0);
-                    }
-            }
+                for (int db = 0; db < DB; ++db) {
+                    const int row0 = 16 * k4 * D;
+                    const s16x4_t both[2] = {lds_read_tr(vb + v_off[db] + row0),
+                                             lds_read_tr(vb + (v_off[db] ^ (kSwz8 << 3)) + 8 * D + row0)};
+                    acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, both), pb[k4],
+                                                                      acc[db], 0, 0, 0);
+                }
         }
         if (more) {
             if (!wave_live) load_tile(t + 1, regs);
@@ -745,10 +723,10 @@ __global__ void __launch_bounds__(kMergeRows * D / 4) merge_kernel(const Plan pl
     constexpr int TPR = D / 4;                      // threads per row
     constexpr int CHUNKS = kTileRows / kMergeRows;  // blocks per (row tile, KV head)
     constexpr int U = 8;                            // splits loaded per batch
-    int part_base = 0, merge_base = 0;
-    const int gi = find_merge_group(plan, blockIdx.x, a.hkv, part_base, merge_base);
-    if (gi < 0) return;
+    const int gi = plan_search<&Group::merge_base>(plan, blockIdx.x);
     const Group g = plan.g[gi];
+    const int part_base = g.part_base, merge_base = g.merge_base;
+    if (g.n_split <= 1) return;
     int li = blockIdx.x - merge_base;
     if (li >= a.hkv * g.n_rt * CHUNKS) return;
     const int chunk = li % CHUNKS;
@@ -806,18 +784,6 @@ __global__ void __launch_bounds__(kMergeRows * D / 4) merge_kernel(const Plan pl
 // one-query (decode) attention: helpers
 // ---------------------------------------------------------------------------------
 constexpr int kDecKeys = kDecTileKeys;
-
-__device__ __forceinline__ int dec_parts(const Group& x, int n_hg) { return x.n_split > 1 ? x.n_split * n_hg : 0; }
-
-__device__ __forceinline__ int find_dec_group(const Plan& plan, int bid, int n_hg, int& part_base) {
-    int gi = 0, part = plan.part0;
-    while (gi + 1 < plan.n_groups && plan.g[gi + 1].item_base <= bid) {
-        part += dec_parts(plan.g[gi], n_hg);
-        ++gi;
-    }
-    part_base = part;
-    return gi;
-}
 
 __device__ __forceinline__ float max_xor16(float x) {
     const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
@@ -927,7 +893,7 @@ __global__ void __launch_bounds__(dec_heads(D) * 64, 1) decode_bf16(const Plan p
     const int c16 = lane & 15, q4 = lane >> 4;   // MFMA column (query / key row) and row group
     const int n_hg = (a.hkv + HW - 1) / HW;
     int part_base;
-    const Group g = plan.g[find_dec_group(plan, blockIdx.x, n_hg, part_base)];
+    const Group g = plan.g[find_group(plan, blockIdx.x, part_base)];
     const int li = blockIdx.x - g.item_base;
     if (li >= g.n_split * n_hg) return;
     const int split = li / n_hg, hg = li - (li / n_hg) * n_hg;
@@ -1227,48 +1193,47 @@ __global__ void __launch_bounds__(dec_heads(D) * 64, 1) decode_bf16(const Plan p
     }
 }
 
-// decode merge: one block per (request, 8 query heads), one float4 of a row per thread
+// decode merge: one block per (request, kMergeRows query heads), one float4 of a
+// row per thread; the (max, sum) pairs and partial rows of up to 8 splits are
+// loaded together before they are combined (streaming log-sum-exp)
 template <int D>
 __global__ void __launch_bounds__(kMergeRows * D / 4) decode_merge(const Plan plan, const Args a) {
     constexpr int TPR = D / 4;
     constexpr int HW = dec_heads(D);
+    constexpr int U = 8;
     const int n_hg = (a.hkv + HW - 1) / HW;
-    const int per_req = (a.hq + kMergeRows - 1) / kMergeRows;
-    // locate the request among the split groups
-    int part = plan.part0, merge = 0, gi = -1;
-    for (int i = 0; i < plan.n_groups; ++i) {
-        const int nb = plan.g[i].n_split > 1 ? per_req : 0;
-        if ((int)blockIdx.x < merge + nb) {
-            gi = i;
-            break;
-        }
-        merge += nb;
-        part += dec_parts(plan.g[i], n_hg);
-    }
-    if (gi < 0) return;
-    const Group g = plan.g[gi];
-    const int qh = ((int)blockIdx.x - merge) * kMergeRows + (int)threadIdx.x / TPR;
+    const Group g = plan.g[plan_search<&Group::merge_base>(plan, blockIdx.x)];
+    if (g.n_split <= 1) return;
+    const int qh = ((int)blockIdx.x - g.merge_base) * kMergeRows + (int)threadIdx.x / TPR;
     const int q4 = (int)threadIdx.x % TPR;
     if (qh >= a.hq) return;
     const int kvh = qh / a.group, c = qh - kvh * a.group;
     const int hg = kvh / HW, prow = (kvh % HW) * 16 + c;
     const int L = g.tok0 + 1;
+    const int n_live = min(g.n_split, (L - g.win + g.split_keys - 1) / g.split_keys);   // non-empty splits
     float M = kNegBig, den = 0.f;
     float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int s = 0; s < g.n_split; ++s) {
-        if (g.win + s * g.split_keys >= L) break;
-        const size_t slot = (size_t)part + (size_t)s * n_hg + hg;
-        const float2 ml = *reinterpret_cast<const float2*>(a.part_ml + (slot * kTileRows + prow) * 2);
-        if (!(ml.y > 0.f)) continue;
-        const float4 v = *reinterpret_cast<const float4*>(a.part_o + (slot * kTileRows + prow) * D + q4 * 4);
-        const float m_new = fmaxf(M, ml.x);
-        const float c_old = __builtin_amdgcn_exp2f(M - m_new), c_new = __builtin_amdgcn_exp2f(ml.x - m_new);
-        num.x = num.x * c_old + c_new * v.x;
-        num.y = num.y * c_old + c_new * v.y;
-        num.z = num.z * c_old + c_new * v.z;
-        num.w = num.w * c_old + c_new * v.w;
-        den = den * c_old + c_new * ml.y;
-        M = m_new;
+    for (int s0 = 0; s0 < n_live; s0 += U) {
+        float2 ml[U];
+        float4 v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const size_t slot = (size_t)g.part_base + (size_t)min(s0 + u, n_live - 1) * n_hg + hg;
+            ml[u] = *reinterpret_cast<const float2*>(a.part_ml + (slot * kTileRows + prow) * 2);
+            v[u] = *reinterpret_cast<const float4*>(a.part_o + (slot * kTileRows + prow) * D + q4 * 4);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (s0 + u >= n_live) break;
+            const float m_new = fmaxf(M, ml[u].x);
+            const float c_old = __builtin_amdgcn_exp2f(M - m_new), c_new = __builtin_amdgcn_exp2f(ml[u].x - m_new);
+            num.x = num.x * c_old + c_new * v[u].x;
+            num.y = num.y * c_old + c_new * v[u].y;
+            num.z = num.z * c_old + c_new * v[u].z;
+            num.w = num.w * c_old + c_new * v[u].w;
+            den = den * c_old + c_new * ml[u].y;
+            M = m_new;
+        }
     }
     const float inv = 1.f / den;
     uint32_t* op = reinterpret_cast<uint32_t*>(static_cast<uint16_t*>(a.o) + ((size_t)g.q_row0 * a.hq + qh) * D + q4 * 4);
@@ -1286,7 +1251,7 @@ __global__ void __launch_bounds__(64) attn_f32(const Plan plan, const Args a) {
     const int lane = threadIdx.x;
     const int bid = blockIdx.x;
     int unused;
-    const Group g = plan.g[find_group(plan, bid, 0, unused)];
+    const Group g = plan.g[find_group(plan, bid, unused)];
     const int li = bid - g.item_base;
     if (li >= g.n_tok * a.hq) return;
     const int toff = li / a.hq, h = li - toff * a.hq;
