@@ -133,6 +133,20 @@ def bench_workload(wl, steps, warmup, stream, with_control=True):
         out["decode_GBps"] = gbs
         out["pct_hbm_peak"] = 100.0 * gbs / PEAK_HBM_GBS
         out["tokens_per_s"] = wl.num_reqs / (out["attn_ms_median"] * 1e-3)
+        # cold: a 1 GiB write between calls evicts the K/V from the 256 MB Infinity Cache
+        scratch = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        cold = []
+        for i in range(max(steps // 4, 5)):
+            scratch.fill_(i & 255)
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            db.attend()
+            b.record(stream)
+            torch.cuda.synchronize()
+            cold.append(a.elapsed_time(b))
+        del scratch
+        out["attn_ms_cold_median"] = float(np.median(cold))
+        out["decode_GBps_cold"] = decode_bytes(wl) / (out["attn_ms_cold_median"] * 1e-3) / 1e9
     else:
         tf = flops_of(wl) / (out["attn_ms_median"] * 1e-3) / 1e12
         out["TFLOPs"] = tf
@@ -188,7 +202,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-extra", action="store_true")
-    ap.add_argument("--configs", default="2,3,4")
+    ap.add_argument("--configs", default="2,3,3u,4")
     ap.add_argument("--calib", action="store_true", help="also run the 256 MiB calibration copy")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -242,11 +256,15 @@ def main():
         calibration_copy()
     if not args.no_extra:
         extra = {"config1": bench_workload(wl, args.steps, args.warmup, stream)}
-        for c in [int(x) for x in args.configs.split(",") if x]:
-            w = W.make_config(c)
-            extra[f"config{c}"] = bench_workload(w, max(args.steps // 2, 10), max(args.warmup // 2, 3), stream)
-            print(f"# config{c}: {json.dumps(extra[f'config{c}'])}", file=sys.stderr, flush=True)
+        for c in [x.strip() for x in args.configs.split(",") if x.strip()]:
+            # "3u": the decode workload with every request's spans private (2.15 GB of
+            # unique K/V, the HBM-bound control of the shared-span decode)
+            w = W.config3(shared=False) if c == "3u" else W.make_config(int(c))
+            name = "config3_unshared" if c == "3u" else f"config{c}"
+            extra[name] = bench_workload(w, max(args.steps // 2, 10), max(args.warmup // 2, 3), stream)
+            print(f"# {name}: {json.dumps(extra[name])}", file=sys.stderr, flush=True)
             del w
+            torch.cuda.empty_cache()
         result["extra"] = extra
     if not args.no_cpu:
         result["cpu_baseline"] = cpu_baseline(wl)
