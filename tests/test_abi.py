@@ -214,3 +214,11 @@ def test_plan_exact_cover_decode_shapes(Hq, Hkv, D):
         assert len({(r, k) for r, k, _ in owners}) == 1, (s, owners)
     if slots:
         assert sorted(slots) == list(range(len(slots)))
+
+
+@pytest.mark.parametrize("dtype", [B.PIC_BF16, B.PIC_F32])
+def test_plan_exact_cover_explicit_windows(dtype):
+    from tests.cases import windows_decode_case, windows_prefill_case
+    wl = windows_prefill_case()
+    assert check_exact_cover(wl, dtype, False) == (16 + 16 + 40 + 37) * 8
+    assert check_exact_cover(windows_decode_case(), dtype, True) == 2 * 32

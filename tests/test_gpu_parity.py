@@ -6,7 +6,7 @@ import torch
 import workloads as W
 from oracle import pic_oracle as O
 from oracle import workload_oracle as WO
-from tests.cases import decode_case
+from tests.cases import decode_case, windows_decode_case, windows_prefill_case
 from tests.gpu_util import assert_close, gpu_run, say, to_np
 
 pytestmark = pytest.mark.gpu
@@ -263,3 +263,12 @@ def test_decode_prerotated_equals_fused():
     torch.cuda.synchronize()
     assert_close(to_np(ctl.o), to_np(fused.o), wl.dtype, "pre-rotated decode vs fused")
     assert_close(to_np(fused.o), WO.run(wl), wl.dtype, "fused decode vs oracle")
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_generalised_windows_prefill(dtype):
+    check(windows_prefill_case(dtype), what=f"generalised windows {dtype}")
+
+
+def test_generalised_windows_decode():
+    check(windows_decode_case(), what="generalised windows decode")

@@ -394,3 +394,50 @@ def test_stored_oracle_fixture():
         got = np.array([o[tuple(i)] for i in ref["index"]])
         assert np.max(np.abs(got - np.array(ref["value"]))) <= 1e-12
         assert abs(o.sum() - ref["sum"]) <= 1e-9
+
+
+# ---- generalised windows (explicit per-span window starts) --------------------------
+
+def test_explicit_windows_equal_flag_windows():
+    # windows given explicitly reproduce the flag-derived ones exactly
+    reqs = [[Sp(10, S), Sp(7, Q, fresh=True), Sp(12, S | Q, fresh=True), Sp(5, P | Q, fresh=True)],
+            [Sp(16, S, key="a"), Sp(9, Q, fresh=True)]]
+    wl = W.small_case("flags", reqs, Hq=4, Hkv=2, D=8, theta=50.0, seed=21)
+    ref = oracle_of(wl)
+    win = []
+    for r in range(wl.num_reqs):
+        sl = slice(wl.cu_spans[r], wl.cu_spans[r + 1])
+        w_tok = O.span_windows(wl.span_start[sl], wl.span_flags[sl], int(wl.seq_lens[r]))
+        win += [int(w_tok[b]) for b in wl.span_start[sl]]
+    wl.span_window = np.array(win, dtype=np.int32)
+    wl.span_flags = wl.span_flags & Q          # flags no longer carry the windows
+    assert np.array_equal(oracle_of(wl), ref)
+
+
+def test_nback_window_equals_subrequest():
+    # a query span whose window starts at the previous document (one-back) sees
+    # exactly what the same tokens see as a request made of those two documents
+    # (without the explicit window the unflagged middle document would keep the first
+    # document's window and the query span would see all 32 tokens)
+    full = W.small_case("nb", [[Sp(12, S), Sp(11, 0), Sp(9, Q, fresh=True)]], Hq=4, Hkv=2, D=8, seed=22)
+    full.span_window = np.array([-1, -1, 12], dtype=np.int32)
+    sub = W.small_case("sub", [[Sp(11, S), Sp(9, Q, fresh=True)]], Hq=4, Hkv=2, D=8, seed=22)
+    k, v = WO.pools_after_write(full)
+    blk = full.block_tables[0]
+    # copy tokens 12..31 of the full request into the sub-request's pool slots
+    ks, vs = WO.pools_after_write(sub)
+    for n in range(20):
+        src = 12 + n
+        ks[sub.block_tables[0][n // 16], :, n % 16] = k[blk[src // 16], :, src % 16]
+        vs[sub.block_tables[0][n // 16], :, n % 16] = v[blk[src // 16], :, src % 16]
+    sub.positions = full.positions[12:32].copy()
+    sub.q = full.q.clone()
+    o_sub = WO.run(sub, pools=(ks, vs))
+    assert np.max(np.abs(oracle_of(full) - o_sub)) <= 1e-13
+
+
+def test_planted_ignored_window_override_is_caught(monkeypatch):
+    orig = O.span_windows
+    monkeypatch.setattr(O, "span_windows", lambda a, b, c, span_window=None: orig(a, b, c, None))
+    with pytest.raises(AssertionError):
+        test_nback_window_equals_subrequest()
