@@ -68,6 +68,17 @@ _sig = {
     "pic_attn_decode": (c_int32, [_P(pic_config), _P(pic_batch_host), _P(pic_batch_dev), _P(pic_rope_table),
                                   c_void_p, c_void_p, c_void_p, c_void_p, c_int32, c_void_p, c_size_t, c_void_p]),
     "pic_plan_debug": (c_int32, [_P(pic_config), _P(pic_batch_host), c_int32, _P(c_int32), c_int32, _P(c_int32)]),
+    # span cache (include/pic_cache.h): host only
+    "pic_sha256": (c_int32, [c_void_p, c_size_t, c_void_p]),
+    "pic_block_hashes": (c_int32, [c_void_p, c_int32, c_int32, c_int32, c_void_p, c_void_p]),
+    "pic_spans_from_blocks": (c_int32, [c_void_p, c_int32, c_int32, c_int32, c_void_p, c_void_p, c_void_p, c_int32,
+                                        _P(c_int32)]),
+    "pic_block_cache_create": (c_int32, [_P(c_void_p)]),
+    "pic_block_cache_destroy": (c_int32, [c_void_p]),
+    "pic_block_cache_lookup": (c_int32, [c_void_p, c_void_p, c_int32, c_void_p, _P(c_int32)]),
+    "pic_block_cache_insert": (c_int32, [c_void_p, c_void_p, c_void_p, c_int32]),
+    "pic_block_cache_erase": (c_int32, [c_void_p, c_void_p, c_int32]),
+    "pic_block_cache_size": (c_int32, [c_void_p, _P(c_int32)]),
 }
 for _name, (_res, _args) in _sig.items():
     _f = getattr(_lib, _name)
@@ -190,3 +201,90 @@ def pic_plan_debug(cfg: pic_config, batch: HostBatch, is_decode: bool) -> np.nda
     _check(_lib.pic_plan_debug(ctypes.byref(cfg), ctypes.byref(batch.c), int(is_decode),
                                out.ctypes.data_as(POINTER(c_int32)), n.value, ctypes.byref(n)))
     return out[: n.value]
+
+
+# ------------------------------------------------------------------------------------
+# span cache (host only): block hashes by the rule of Sec. 3.1.1 eq. (1), span
+# boundaries from cache hits, and the hash -> block map
+# ------------------------------------------------------------------------------------
+
+def _i32(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+def _u8(a) -> np.ndarray:
+    return np.ascontiguousarray(np.frombuffer(a, dtype=np.uint8) if isinstance(a, (bytes, bytearray)) else a,
+                                dtype=np.uint8)
+
+
+def pic_sha256(data: bytes) -> bytes:
+    buf = np.frombuffer(bytes(data), dtype=np.uint8)
+    out = np.zeros(32, dtype=np.uint8)
+    _check(_lib.pic_sha256(buf.ctypes.data if len(buf) else None, len(buf), out.ctypes.data))
+    return out.tobytes()
+
+
+def pic_block_hashes(tokens, ssep_token: int, pdep_token: int, seed: bytes) -> np.ndarray:
+    """uint8 [len(tokens)//16][32]: the hash of every full block."""
+    tok = _i32(tokens)
+    sd = _u8(seed)
+    if sd.size != 32:
+        raise ValueError("seed must be 32 bytes")
+    out = np.zeros((len(tok) // 16, 32), dtype=np.uint8)
+    _check(_lib.pic_block_hashes(tok.ctypes.data, len(tok), int(ssep_token), int(pdep_token), sd.ctypes.data,
+                                 out.ctypes.data))
+    return out
+
+
+def pic_spans_from_blocks(tokens, ssep_token: int, pdep_token: int, hit):
+    """(span_start, span_flags) int32 arrays for pic_attn_prefill from per-block hits."""
+    tok = _i32(tokens)
+    h = np.ascontiguousarray(np.asarray(hit, dtype=bool).astype(np.uint8))
+    if h.size != len(tok) // 16:
+        raise ValueError("hit needs one entry per full block")
+    cap = -(-len(tok) // 16) + 1
+    start = np.zeros(cap, dtype=np.int32)
+    flags = np.zeros(cap, dtype=np.int32)
+    n = c_int32(0)
+    _check(_lib.pic_spans_from_blocks(tok.ctypes.data, len(tok), int(ssep_token), int(pdep_token),
+                                      h.ctypes.data if h.size else None, start.ctypes.data, flags.ctypes.data, cap,
+                                      ctypes.byref(n)))
+    return start[: n.value].copy(), flags[: n.value].copy()
+
+
+def pic_block_cache_create() -> int:
+    handle = c_void_p()
+    _check(_lib.pic_block_cache_create(ctypes.byref(handle)))
+    return handle.value
+
+
+def pic_block_cache_destroy(cache: int) -> None:
+    _check(_lib.pic_block_cache_destroy(cache))
+
+
+def pic_block_cache_lookup(cache: int, hashes):
+    """(block_ids int32 [n] with -1 for a miss, number of hits)."""
+    hs = _u8(hashes).reshape(-1, 32)
+    ids = np.zeros(len(hs), dtype=np.int32)
+    hits = c_int32(0)
+    _check(_lib.pic_block_cache_lookup(cache, hs.ctypes.data, len(hs), ids.ctypes.data, ctypes.byref(hits)))
+    return ids, hits.value
+
+
+def pic_block_cache_insert(cache: int, hashes, block_ids) -> None:
+    hs = _u8(hashes).reshape(-1, 32)
+    ids = _i32(block_ids)
+    if len(ids) != len(hs):
+        raise ValueError("one block id per hash")
+    _check(_lib.pic_block_cache_insert(cache, hs.ctypes.data, ids.ctypes.data, len(hs)))
+
+
+def pic_block_cache_erase(cache: int, hashes) -> None:
+    hs = _u8(hashes).reshape(-1, 32)
+    _check(_lib.pic_block_cache_erase(cache, hs.ctypes.data, len(hs)))
+
+
+def pic_block_cache_size(cache: int) -> int:
+    n = c_int32(0)
+    _check(_lib.pic_block_cache_size(cache, ctypes.byref(n)))
+    return n.value

@@ -14,7 +14,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libpic_attn.so")
-SOURCES = [os.path.join(CSRC, "pic_kernels.hip"), os.path.join(CSRC, "pic_host.cpp")]
+SOURCES = [os.path.join(CSRC, "pic_kernels.hip"), os.path.join(CSRC, "pic_host.cpp"),
+           os.path.join(CSRC, "pic_cache.cpp")]
 
 # -packed-fp32-ops is a device feature: hipcc's host pass warns that it does not
 # know it, which is harmless.

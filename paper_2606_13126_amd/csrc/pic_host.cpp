@@ -332,6 +332,10 @@ pic_status run_attention(const pic_config* c, const pic_batch_host* b, const pic
 
 }  // namespace
 
+namespace pic {
+pic_status host_fail(pic_status st, const char* msg) { return fail(st, msg); }
+}  // namespace pic
+
 extern "C" {
 
 int32_t pic_version(void) { return 100; }

@@ -91,6 +91,9 @@ struct Args {
     int32_t group;            // G = hq / hkv
 };
 
+// Records msg as the thread's last error (pic_last_error) and returns st.
+int32_t host_fail(int32_t st, const char* msg);
+
 // Launchers implemented in pic_kernels.hip.  Each returns a hipError_t value.
 int launch_kv_write(int dtype, int hkv, int d, void* k_pool, void* v_pool, const void* k_new,
                     const void* v_new, const int32_t* slots, int n, void* stream);

@@ -18,7 +18,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
 def declared_functions():
-    src = open(os.path.join(ROOT, "include", "pic_attn.h")).read()
+    src = "".join(open(os.path.join(ROOT, "include", h)).read() for h in ("pic_attn.h", "pic_cache.h"))
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
     return sorted(set(re.findall(r"\b(pic_[a-z_0-9]+)\s*\(", src)))
 
