@@ -44,6 +44,13 @@ __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b) {
                                            false);
 }
 
+// c + a.lo + a.hi for a pair of bf16 values (a dot product with (1, 1), one
+// accumulate-in-place instruction)
+__device__ __forceinline__ float sum2_bf16(uint32_t a, float c) {
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a), __builtin_bit_cast(bf16x2_t, 0x3f803f80u), c,
+                                           false);
+}
+
 // Round two floats to bf16 (round to nearest even) and pack them, lo first.
 __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
     bf16x2_t v = {(__bf16)lo, (__bf16)hi};
@@ -640,8 +647,10 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
                 for (int db = 0; db < DB; ++db) acc[db] *= alpha;
                 m_run = m_new;
             }
-            // probabilities: fp32 for the row sum, bf16 for P V
+            // probabilities rounded to bf16 for P V; the row sum adds exactly those, two
+            // at a time
             bf16x8_t pb[2 * NH];
+            float part[2] = {0.f, 0.f};
 #pragma unroll
             for (int mb = 0; mb < NH; ++mb)
 #pragma unroll
@@ -651,11 +660,12 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
                     for (int m = 0; m < 4; ++m) {
                         const float p0 = __builtin_amdgcn_exp2f(s[mb][8 * k2 + 2 * m] - m_run);
                         const float p1 = __builtin_amdgcn_exp2f(s[mb][8 * k2 + 2 * m + 1] - m_run);
-                        l_run += p0 + p1;
                         w[m] = pack_bf16(p0, p1);
+                        part[m & 1] = sum2_bf16(w[m], part[m & 1]);
                     }
                     pb[2 * mb + k2] = __builtin_bit_cast(bf16x8_t, w);
                 }
+            l_run += part[0] + part[1];
             if (more) load_tile(t + 1, regs);
             // ---- O^T += V^T P^T, 16 keys per step, the DB independent accumulators in turn
 #pragma unroll
