@@ -172,6 +172,38 @@ def bench_workload(wl, steps, warmup, stream, with_control=True):
     return out
 
 
+def bench_offload(steps, stream, n_blocks=4096, hkv=8, d=128):
+    """Block offload (pic_blocks_gather / pic_blocks_scatter): 4096 bf16 blocks of 8 kv
+    heads x 16 tokens x 128 dims (64 KiB of K+V per block, 256 MiB in all) moved to
+    pinned host memory and back under permuted ids, and pool-to-pool on the device.
+    A DMA copy of one dense buffer of the same size is timed beside them."""
+    from paper_2606_13126_amd import _binding as B
+    cfg = B.make_config(4 * hkv, hkv, d)
+    nb = n_blocks + 512
+    page = (hkv, 16, d)
+    k = torch.randn((nb,) + page, device="cuda").to(torch.bfloat16)
+    v = torch.randn_like(k)
+    ids = torch.randperm(nb, device="cuda")[:n_blocks].to(torch.int32)
+    hk = torch.empty((n_blocks,) + page, dtype=torch.bfloat16, pin_memory=True)
+    hv = torch.empty((n_blocks,) + page, dtype=torch.bfloat16, pin_memory=True)
+    dk = torch.empty((n_blocks,) + page, dtype=torch.bfloat16, device="cuda")
+    dv = torch.empty_like(dk)
+    nbytes = 2 * hk.numel() * hk.element_size()
+    out = {"blocks": n_blocks, "bytes": nbytes}
+    n = max(steps // 5, 5)
+    for name, fn in (("gather_to_host", lambda: B.pic_blocks_gather(cfg, k, v, ids, hk, hv)),
+                     ("scatter_from_host", lambda: B.pic_blocks_scatter(cfg, k, v, ids, hk, hv)),
+                     ("gather_on_device", lambda: B.pic_blocks_gather(cfg, k, v, ids, dk, dv)),
+                     ("dma_dense_to_host", lambda: (hk.copy_(dk, non_blocking=True),
+                                                   hv.copy_(dv, non_blocking=True)))):
+        ms = float(np.median(timed(fn, n, 2, stream)))
+        out[name + "_ms"] = ms
+        out[name + "_GBps"] = nbytes / (ms * 1e-3) / 1e9
+    del k, v, hk, hv, dk, dv
+    torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline(wl, budget_s=12.0):
     """The fp64 oracle (kv_write + prefill) on this host, repeated for about budget_s."""
     from oracle import workload_oracle as WO
@@ -265,6 +297,8 @@ def main():
             print(f"# {name}: {json.dumps(extra[name])}", file=sys.stderr, flush=True)
             del w
             torch.cuda.empty_cache()
+        extra["offload"] = bench_offload(args.steps, stream)
+        print(f"# offload: {json.dumps(extra['offload'])}", file=sys.stderr, flush=True)
         result["extra"] = extra
     if not args.no_cpu:
         result["cpu_baseline"] = cpu_baseline(wl)

@@ -141,6 +141,27 @@ pic_status pic_kv_write(const pic_config* cfg, void* k_pool, void* v_pool, int32
                         const void* k_new, const void* v_new, const int32_t* slot_mapping, int32_t n,
                         void* stream);
 
+/* Move whole cache blocks between the pool and another buffer, e.g. to offload
+ * them to host memory and bring them back (Sec. 3.2.3, "Native Offloading
+ * Compatibility": the blocks hold unrotated keys, so they move between memory
+ * tiers with no position bookkeeping and may come back under different block ids
+ * and be read at any logical offset).  Block b is the K page run
+ * k_pool[b][0..Hkv)[16][D] and the same run of V (Hkv*16*D elements each).
+ *  pic_blocks_gather:  dst_k[i] <- k_pool[block_ids[i]], dst_v[i] <- v_pool[block_ids[i]]
+ *  pic_blocks_scatter: k_pool[block_ids[i]] <- src_k[i], v_pool[block_ids[i]] <- src_v[i]
+ * for i < n.  dst/src are [n][Hkv][16][D] in cfg->dtype, in device memory or in
+ * pinned host memory (hipHostMalloc, e.g. a torch tensor created with
+ * pin_memory=True); other host memory, managed memory and addresses that are not
+ * 16-byte aligned are rejected with PIC_EINVAL.  block_ids is
+ * DEVICE [n] and trusted (ids in [0, num_blocks); distinct for a scatter).  One
+ * kernel on `stream` copies 16-byte chunks (host buffers are read or written across
+ * the host link by the kernel itself); the copies are bit-exact. */
+pic_status pic_blocks_gather(const pic_config* cfg, const void* k_pool, const void* v_pool, int32_t num_blocks,
+                             const int32_t* block_ids, int32_t n, void* dst_k, void* dst_v, void* stream);
+pic_status pic_blocks_scatter(const pic_config* cfg, void* k_pool, void* v_pool, int32_t num_blocks,
+                              const int32_t* block_ids, int32_t n, const void* src_k, const void* src_v,
+                              void* stream);
+
 /* Workspace bytes that pic_attn_prefill (is_decode = 0) or pic_attn_decode
  * (is_decode = 1) needs for this configuration and batch (split-KV partial
  * results).  May be 0. */

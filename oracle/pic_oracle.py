@@ -141,6 +141,23 @@ def gather(pool: np.ndarray, block_row: np.ndarray, n_tokens: int, kv_head: int)
     return np.asarray(pool[block_row[n // BLOCK], kv_head, n % BLOCK, :], dtype=np.float64)
 
 
+def blocks_gather(pool: np.ndarray, block_ids: Sequence[int]) -> np.ndarray:
+    """Copy out whole cache blocks (Sec. 3.2.3, offloading): result[i] = pool[block_ids[i]],
+    shape [n][Hkv][16][D], same dtype (bit-exact).  The blocks carry unrotated keys, so
+    nothing about their positions travels with them."""
+    out = np.empty((len(block_ids),) + pool.shape[1:], dtype=pool.dtype)
+    for i, b in enumerate(block_ids):
+        out[i] = pool[int(b)]
+    return out
+
+
+def blocks_scatter(pool: np.ndarray, block_ids: Sequence[int], src: np.ndarray) -> None:
+    """Bring blocks back (Sec. 3.2.3): pool[block_ids[i]] = src[i], in place; the ids may
+    differ from the ones the blocks were gathered from."""
+    for i, b in enumerate(block_ids):
+        pool[int(b)] = src[i]
+
+
 # -------------------------------------------------------------------------------------
 # Attention
 # -------------------------------------------------------------------------------------

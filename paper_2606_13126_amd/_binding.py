@@ -62,6 +62,10 @@ _sig = {
                                   c_void_p]),
     "pic_kv_write": (c_int32, [_P(pic_config), c_void_p, c_void_p, c_int32, c_void_p, c_void_p, c_void_p, c_int32,
                                c_void_p]),
+    "pic_blocks_gather": (c_int32, [_P(pic_config), c_void_p, c_void_p, c_int32, c_void_p, c_int32, c_void_p,
+                                    c_void_p, c_void_p]),
+    "pic_blocks_scatter": (c_int32, [_P(pic_config), c_void_p, c_void_p, c_int32, c_void_p, c_int32, c_void_p,
+                                     c_void_p, c_void_p]),
     "pic_workspace_size": (c_int32, [_P(pic_config), _P(pic_batch_host), c_int32, _P(c_size_t)]),
     "pic_attn_prefill": (c_int32, [_P(pic_config), _P(pic_batch_host), _P(pic_batch_dev), _P(pic_rope_table),
                                    c_void_p, c_void_p, c_void_p, c_void_p, c_int32, c_void_p, c_size_t, c_void_p]),
@@ -170,6 +174,20 @@ def pic_rope_rotate(cfg: pic_config, x, positions, table=None, stream=None) -> N
 def pic_kv_write(cfg: pic_config, k_pool, v_pool, k_new, v_new, slot_mapping, stream=None) -> None:
     _check(_lib.pic_kv_write(ctypes.byref(cfg), _ptr(k_pool), _ptr(v_pool), int(k_pool.shape[0]), _ptr(k_new),
                              _ptr(v_new), _ptr(slot_mapping), int(k_new.shape[0]), _stream(stream)))
+
+
+def pic_blocks_gather(cfg: pic_config, k_pool, v_pool, block_ids, dst_k, dst_v, stream=None) -> None:
+    """dst_k[i], dst_v[i] <- pool block block_ids[i]; dst may be pinned host memory."""
+    _check(_lib.pic_blocks_gather(ctypes.byref(cfg), _ptr(k_pool), _ptr(v_pool), int(k_pool.shape[0]),
+                                  _ptr(block_ids), int(block_ids.shape[0]), _ptr(dst_k), _ptr(dst_v),
+                                  _stream(stream)))
+
+
+def pic_blocks_scatter(cfg: pic_config, k_pool, v_pool, block_ids, src_k, src_v, stream=None) -> None:
+    """Pool block block_ids[i] <- src_k[i], src_v[i]; src may be pinned host memory."""
+    _check(_lib.pic_blocks_scatter(ctypes.byref(cfg), _ptr(k_pool), _ptr(v_pool), int(k_pool.shape[0]),
+                                   _ptr(block_ids), int(block_ids.shape[0]), _ptr(src_k), _ptr(src_v),
+                                   _stream(stream)))
 
 
 def pic_workspace_size(cfg: pic_config, batch: HostBatch, is_decode: bool) -> int:

@@ -387,6 +387,64 @@ pic_status pic_kv_write(const pic_config* cfg, void* k_pool, void* v_pool, int32
                       "kv_write launch");
 }
 
+// A pointer the kernels can dereference: device memory as it is, pinned host memory
+// (hipHostMalloc) through its device mapping.  Anything else -- pageable host memory,
+// managed memory -- is rejected, since a kernel touching it could fault.
+static pic_status kernel_view(const void* p, const char* what, void** out) {
+    hipPointerAttribute_t at{};
+    if (hipPointerGetAttributes(&at, p) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(PIC_EINVAL, std::string(what) + " is neither device memory nor pinned host memory");
+    }
+    if (at.type == hipMemoryTypeDevice) {
+        *out = const_cast<void*>(p);
+        return PIC_OK;
+    }
+    unsigned int flags = 0;
+    if (at.type == hipMemoryTypeHost && at.devicePointer != nullptr &&
+        hipHostGetFlags(&flags, const_cast<void*>(p)) == hipSuccess) {
+        *out = at.devicePointer;
+        return PIC_OK;
+    }
+    (void)hipGetLastError();
+    return fail(PIC_EINVAL, std::string(what) + " is neither device memory nor pinned host memory");
+}
+
+static pic_status blocks_copy(const pic_config* cfg, void* k_pool, void* v_pool, int32_t num_blocks,
+                              const int32_t* block_ids, int32_t n, void* k_buf, void* v_buf, bool to_pool,
+                              void* stream) {
+    pic_status st = check_config(cfg);
+    if (st) return st;
+    if (n < 0 || num_blocks < 0) return fail(PIC_EINVAL, "n and num_blocks must be >= 0");
+    if (n == 0) return PIC_OK;
+    if (!k_pool || !v_pool || !k_buf || !v_buf || !block_ids) return fail(PIC_EINVAL, "NULL buffer");
+    if (num_blocks == 0) return fail(PIC_EINVAL, "empty pool");
+    // one workgroup of 256 lanes per block: the grid's lane count must stay below 2^32
+    if (n >= (1 << 24)) return fail(PIC_EINVAL, "n must be < 2^24 blocks per call");
+    void *kb = nullptr, *vb = nullptr;
+    if ((st = kernel_view(k_buf, to_pool ? "src_k" : "dst_k", &kb))) return st;
+    if ((st = kernel_view(v_buf, to_pool ? "src_v" : "dst_v", &vb))) return st;
+    // the kernel moves 16-byte chunks
+    for (const void* p : {(const void*)k_pool, (const void*)v_pool, (const void*)kb, (const void*)vb})
+        if (reinterpret_cast<uintptr_t>(p) % 16) return fail(PIC_EINVAL, "pool and buffer addresses must be 16-byte aligned");
+    return hip_status(pic::launch_blocks_copy(cfg->dtype, cfg->num_kv_heads, cfg->head_dim, k_pool, v_pool, kb, vb,
+                                              block_ids, n, to_pool, stream),
+                      "blocks_copy launch");
+}
+
+pic_status pic_blocks_gather(const pic_config* cfg, const void* k_pool, const void* v_pool, int32_t num_blocks,
+                             const int32_t* block_ids, int32_t n, void* dst_k, void* dst_v, void* stream) {
+    return blocks_copy(cfg, const_cast<void*>(k_pool), const_cast<void*>(v_pool), num_blocks, block_ids, n, dst_k,
+                       dst_v, false, stream);
+}
+
+pic_status pic_blocks_scatter(const pic_config* cfg, void* k_pool, void* v_pool, int32_t num_blocks,
+                              const int32_t* block_ids, int32_t n, const void* src_k, const void* src_v,
+                              void* stream) {
+    return blocks_copy(cfg, k_pool, v_pool, num_blocks, block_ids, n, const_cast<void*>(src_k),
+                       const_cast<void*>(src_v), true, stream);
+}
+
 pic_status pic_workspace_size(const pic_config* cfg, const pic_batch_host* batch, int32_t is_decode, size_t* bytes) {
     pic_status st = check_config(cfg);
     if (st) return st;

@@ -98,6 +98,8 @@ int32_t host_fail(int32_t st, const char* msg);
 int launch_kv_write(int dtype, int hkv, int d, void* k_pool, void* v_pool, const void* k_new,
                     const void* v_new, const int32_t* slots, int n, void* stream);
 int launch_rope_table(int dtype, int d, double theta, int n_pos, float* table, void* stream);
+int launch_blocks_copy(int dtype, int hkv, int d, void* k_pool, void* v_pool, void* k_buf, void* v_buf,
+                       const int32_t* block_ids, int n, bool to_pool, void* stream);
 int launch_rope_rotate(int dtype, int style, int d, double theta, const float* table, int rope_len, void* x,
                        int n, int heads, const int32_t* positions, void* stream);
 int launch_attention(int dtype, int style, int d, bool rope, const Plan& plan, const Args& args, void* stream);

@@ -132,6 +132,32 @@ __global__ void __launch_bounds__(256) kv_write_kernel(u32x4_t* __restrict__ k_p
 }
 
 // ---------------------------------------------------------------------------------
+// blocks_copy: one workgroup per cache block, 16-byte chunks of its K and V page
+// runs between the pool and a dense [n][page] buffer (gather: pool -> buffer,
+// scatter: buffer -> pool).
+// ---------------------------------------------------------------------------------
+__global__ void __launch_bounds__(256) blocks_copy_kernel(u32x4_t* __restrict__ k_pool, u32x4_t* __restrict__ v_pool,
+                                                          u32x4_t* __restrict__ k_buf, u32x4_t* __restrict__ v_buf,
+                                                          const int32_t* __restrict__ block_ids, int64_t chunks,
+                                                          bool to_pool) {
+    const int64_t i = blockIdx.x;
+    const int64_t b = block_ids[i];
+    u32x4_t* pk = k_pool + b * chunks;
+    u32x4_t* pv = v_pool + b * chunks;
+    u32x4_t* bk = k_buf + i * chunks;
+    u32x4_t* bv = v_buf + i * chunks;
+    for (int64_t c = threadIdx.x; c < chunks; c += blockDim.x) {
+        if (to_pool) {
+            pk[c] = bk[c];
+            pv[c] = bv[c];
+        } else {
+            bk[c] = pk[c];
+            bv[c] = pv[c];
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------------
 // rope_table: entry [p][i] from cos/sin(p * omega_i) in float64, stored as float32
 // (cos, sin) or as bf16 (cos, -sin, sin, cos).
 // ---------------------------------------------------------------------------------
@@ -1394,6 +1420,16 @@ int launch_kv_write(int dtype, int hkv, int d, void* k_pool, void* v_pool, const
                        static_cast<u32x4_t*>(k_pool), static_cast<u32x4_t*>(v_pool),
                        static_cast<const u32x4_t*>(k_new), static_cast<const u32x4_t*>(v_new), slots, n_chunks,
                        chunks_per_head, hkv);
+    return hipGetLastError();
+}
+
+int launch_blocks_copy(int dtype, int hkv, int d, void* k_pool, void* v_pool, void* k_buf, void* v_buf,
+                       const int32_t* block_ids, int n, bool to_pool, void* stream) {
+    if (n == 0) return hipSuccess;
+    const int64_t chunks = (int64_t)hkv * kBlock * d * (dtype == 1 ? 4 : 2) / 16;
+    hipLaunchKernelGGL(blocks_copy_kernel, dim3((unsigned)n), dim3(256), 0, (hipStream_t)stream,
+                       static_cast<u32x4_t*>(k_pool), static_cast<u32x4_t*>(v_pool), static_cast<u32x4_t*>(k_buf),
+                       static_cast<u32x4_t*>(v_buf), block_ids, chunks, to_pool);
     return hipGetLastError();
 }
 

@@ -25,7 +25,8 @@ def declared_functions():
 
 def test_header_declares_the_boundary():
     names = declared_functions()
-    for required in ("pic_kv_write", "pic_attn_prefill", "pic_attn_decode", "pic_workspace_size"):
+    for required in ("pic_kv_write", "pic_attn_prefill", "pic_attn_decode", "pic_workspace_size",
+                     "pic_blocks_gather", "pic_blocks_scatter"):
         assert required in names
 
 
@@ -97,6 +98,16 @@ def test_errors_before_any_hip_call():
     assert lib.pic_kv_write(ctypes.byref(P.make_config(4, 3, 64)), fake, fake, 4, fake, fake, fake, 3,
                             None) == B.PIC_EINVAL
     assert lib.pic_rope_rotate(ctypes.byref(cfg), None, None, 5, 2, fake, None) == B.PIC_EINVAL
+    # block offload: NULL buffers, negative counts, empty pool, oversized n, bad config
+    assert lib.pic_blocks_gather(ctypes.byref(cfg), fake, fake, 4, fake, 3, None, fake, None) == B.PIC_EINVAL
+    assert lib.pic_blocks_scatter(ctypes.byref(cfg), fake, fake, 4, None, 3, fake, fake, None) == B.PIC_EINVAL
+    assert lib.pic_blocks_gather(ctypes.byref(cfg), fake, fake, 4, fake, -1, fake, fake, None) == B.PIC_EINVAL
+    assert lib.pic_blocks_gather(ctypes.byref(cfg), fake, fake, 0, fake, 2, fake, fake, None) == B.PIC_EINVAL
+    assert lib.pic_blocks_scatter(ctypes.byref(cfg), fake, fake, 4, fake, 1 << 24, fake, fake, None) == B.PIC_EINVAL
+    assert lib.pic_blocks_gather(ctypes.byref(P.make_config(4, 3, 64)), fake, fake, 4, fake, 2, fake, fake,
+                                 None) == B.PIC_EINVAL
+    # nothing to move: success without a launch
+    assert lib.pic_blocks_gather(ctypes.byref(cfg), None, None, 0, None, 0, None, None, None) == B.PIC_OK
     wl = W.config0()
     hb = batch_of(wl)
     dev = B.pic_batch_dev(16, 1, 16)   # max_blocks 1 < 10 blocks of the request

@@ -298,6 +298,51 @@ def test_kv_write_scatter():
     assert (kp == -1).sum() == kp.size - 2 * 2 * 3
 
 
+# ---- block offload (Sec. 3.2.3) -------------------------------------------------------
+
+def test_blocks_gather_scatter_index_order():
+    # every element of a tiny pool encodes its own (block, head, offset, dim): a swapped
+    # or transposed index in the copies shows up as a wrong code
+    nb, hkv, d = 6, 3, 5
+    b, h, o, e = np.meshgrid(np.arange(nb), np.arange(hkv), np.arange(16), np.arange(d), indexing="ij")
+    pool = (b * 10000 + h * 1000 + o * 10 + e).astype(np.int32)
+    ids = [4, 0, 4, 2]
+    out = O.blocks_gather(pool, ids)
+    assert out.shape == (4, hkv, 16, d)
+    for i, bi in enumerate(ids):
+        for hh in range(hkv):
+            for oo in range(16):
+                for ee in range(d):
+                    assert out[i, hh, oo, ee] == bi * 10000 + hh * 1000 + oo * 10 + ee
+    dst = np.full_like(pool, -1)
+    O.blocks_scatter(dst, [5, 1, 3], out[[0, 1, 3]])
+    assert np.array_equal(dst[5], pool[4]) and np.array_equal(dst[1], pool[0]) and np.array_equal(dst[3], pool[2])
+    assert (dst[[0, 2, 4]] == -1).all()
+
+
+def test_offload_and_reload_under_new_ids_keeps_outputs():
+    # Sec. 3.2.3: blocks leave the pool (here to a bf16-width byte buffer standing in for
+    # host memory), come back under different ids into a pool whose other blocks hold
+    # garbage, and the block table is the only thing updated: outputs are unchanged
+    wl = W.config0()
+    k, v = WO.pools_after_write(wl)
+    o0 = oracle_of(wl)
+    used = np.unique(wl.block_tables[wl.block_tables >= 0])
+    host_k = O.blocks_gather(k, used).tobytes()
+    host_v = O.blocks_gather(v, used).tobytes()
+    nb = k.shape[0] + 7
+    new_ids = RNG.permutation(nb)[:len(used)]
+    k2 = RNG.standard_normal((nb,) + k.shape[1:])
+    v2 = RNG.standard_normal((nb,) + v.shape[1:])
+    shape = (len(used),) + k.shape[1:]
+    O.blocks_scatter(k2, new_ids, np.frombuffer(host_k, dtype=k.dtype).reshape(shape))
+    O.blocks_scatter(v2, new_ids, np.frombuffer(host_v, dtype=v.dtype).reshape(shape))
+    remap = np.full(k.shape[0], -1, dtype=np.int64)
+    remap[used] = new_ids
+    wl.block_tables = np.where(wl.block_tables >= 0, remap[np.maximum(wl.block_tables, 0)], -1).astype(np.int32)
+    assert np.array_equal(o0, WO.run(wl, pools=(k2, v2)))
+
+
 def test_span_windows_rule():
     w = O.span_windows([0, 5, 9, 14, 20], [S, 0, P, 0, S], 25)
     assert list(w) == [0] * 5 + [0] * 4 + [0] * 5 + [0] * 6 + [20] * 5
