@@ -74,6 +74,15 @@ typedef struct pic_config {
     int32_t k_prerotated;  /* 0: the pool holds unrotated K and q is unrotated (the method);
                               1: both are already rotated and no RoPE is applied (the
                                  baseline FlashAttention of Sec. 3.2.2, for comparison) */
+    /* RoPE variants of the models the method applies to (Sec. 3.2.1 takes the model's
+     * own rotary embedding).  rotary_dim R: only the first R elements of q and k turn
+     * (partial rotary), 0 means R = D; even, 2 <= R <= D, and R < D only with
+     * PIC_ROPE_GPTJ (pairs 2i, 2i+1 for i < R/2).  inv_freq: HOST [R/2] frequencies
+     * omega_i (radians per position), finite, read during each call that takes cfg --
+     * scaled-RoPE variants (position interpolation, NTK, Llama-3-style band scaling)
+     * change only these; NULL means omega_i = theta^(-2i/R). */
+    const double* inv_freq;
+    int32_t rotary_dim;
 } pic_config;
 
 /* Span structure of a batch (HOST).  Request r has seq_lens[r] >= 1 tokens
@@ -102,7 +111,8 @@ typedef struct pic_batch_dev {
 
 /* Optional cos/sin table (the paper's cos_sin lookup, Sec. 3.2.2): one 8-byte entry
  * per (position p in [0, len), pair i in [0, D/2)), from cos/sin(p*omega_i) computed
- * in float64.  PIC_F32 tables hold (cos, sin) as two float32; PIC_BF16 tables hold
+ * in float64 (omega_i = 0 for pairs past rotary_dim).  A table belongs to the
+ * frequencies of the cfg that built it.  PIC_F32 tables hold (cos, sin) as two float32; PIC_BF16 tables hold
  * (cos, -sin, sin, cos) as four bf16, so that the kernel rotates a pair (x, y) with
  * two 2-element dot products.  Built by pic_rope_table_build for cfg->dtype.
  * Positions outside [0, len), and every position when data is NULL, are rotated

@@ -44,27 +44,34 @@ BLOCK = 16
 # -------------------------------------------------------------------------------------
 
 def rope_inv_freq(head_dim: int, theta: float) -> np.ndarray:
-    """omega_i = theta^(-2i/D), i = 0 .. D/2-1, in float64."""
+    """omega_i = theta^(-2i/D), i = 0 .. D/2-1, in float64 (D: the rotated width)."""
     i = np.arange(head_dim // 2, dtype=np.float64)
     return np.power(float(theta), -2.0 * i / head_dim)
 
 
-def rope(x: np.ndarray, pos: np.ndarray, theta: float, style: str = "neox") -> np.ndarray:
+def rope(x: np.ndarray, pos: np.ndarray, theta: float, style: str = "neox",
+         inv_freq: Optional[Sequence[float]] = None, rotary_dim: Optional[int] = None) -> np.ndarray:
     """Rotate the last axis of ``x`` (float64) by R_p, p = ``pos`` broadcast over the
-    leading axes.  NeoX pairs element i with i + D/2; GPT-J pairs 2i with 2i+1; pair i
-    turns by the angle p * omega_i."""
+    leading axes.  Only the first R = ``rotary_dim`` (default: all D) elements turn;
+    the rest pass through.  Within them NeoX pairs element i with i + R/2, GPT-J pairs
+    2i with 2i+1, and pair i turns by the angle p * omega_i, omega_i = theta^(-2i/R)
+    unless ``inv_freq`` (R/2 values) gives the frequencies (scaled RoPE variants)."""
     x = np.asarray(x, dtype=np.float64)
     D = x.shape[-1]
-    ang = np.asarray(pos, dtype=np.float64)[..., None] * rope_inv_freq(D, theta)
+    R = D if rotary_dim is None else int(rotary_dim)
+    om = rope_inv_freq(R, theta) if inv_freq is None else np.asarray(inv_freq, dtype=np.float64)
+    assert om.shape == (R // 2,)
+    ang = np.asarray(pos, dtype=np.float64)[..., None] * om
     c, s = np.cos(ang), np.sin(ang)
+    y = x.copy()
     if style == "neox":
-        a, b = x[..., : D // 2], x[..., D // 2:]
-        return np.concatenate([a * c - b * s, b * c + a * s], axis=-1)
+        a, b = x[..., : R // 2], x[..., R // 2:R]
+        y[..., :R] = np.concatenate([a * c - b * s, b * c + a * s], axis=-1)
+        return y
     if style == "gptj":
-        a, b = x[..., 0::2], x[..., 1::2]
-        y = np.empty_like(x)
-        y[..., 0::2] = a * c - b * s
-        y[..., 1::2] = b * c + a * s
+        a, b = x[..., 0:R:2], x[..., 1:R:2]
+        y[..., 0:R:2] = a * c - b * s
+        y[..., 1:R:2] = b * c + a * s
         return y
     raise ValueError(f"unknown rope style {style!r}")
 
@@ -178,16 +185,17 @@ def _attend(qr: np.ndarray, kr: np.ndarray, v: np.ndarray, t: np.ndarray, w: np.
 
 def _attend_request(q_rows: np.ndarray, q_idx: np.ndarray, k_pool, v_pool, block_row, seq_len,
                     pos_row: np.ndarray, w_tok: np.ndarray, num_kv_heads: int, theta: float,
-                    scale: float, style: str, chunk: int = 512) -> np.ndarray:
+                    scale: float, style: str, chunk: int = 512, rope_kw: Optional[dict] = None) -> np.ndarray:
     """q_rows [T][Hq][D] at sequence indices q_idx of one request -> O [T][Hq][D]."""
     T, Hq, D = q_rows.shape
     G = Hq // num_kv_heads
+    rk = rope_kw or {}
     out = np.empty((T, Hq, D), dtype=np.float64)
     if T == 0:
         return out
     hi = int(q_idx.max()) + 1                 # keys past the last query are never visible
     for g in range(num_kv_heads):
-        kr = rope(gather(k_pool, block_row, hi, g), pos_row[:hi], theta, style)
+        kr = rope(gather(k_pool, block_row, hi, g), pos_row[:hi], theta, style, **rk)
         v = gather(v_pool, block_row, hi, g)
         for c0 in range(0, T, chunk):
             sl = slice(c0, min(T, c0 + chunk))
@@ -197,7 +205,7 @@ def _attend_request(q_rows: np.ndarray, q_idx: np.ndarray, k_pool, v_pool, block
             top = int(t.max()) + 1
             for hl in range(G):
                 h = g * G + hl
-                qr = rope(np.asarray(q_rows[sl, h, :], dtype=np.float64), pos_row[t], theta, style)
+                qr = rope(np.asarray(q_rows[sl, h, :], dtype=np.float64), pos_row[t], theta, style, **rk)
                 out[sl, h, :] = _attend(qr, kr[lo:top], v[lo:top], t - lo, w - lo, scale)
     return out
 
@@ -208,12 +216,13 @@ def _scale(head_dim: int, softmax_scale: float) -> float:
 
 def prefill(q, k_pool, v_pool, block_tables, positions, seq_lens, cu_spans, span_start, span_flags,
             num_kv_heads: int, theta: float, softmax_scale: float = 0.0, style: str = "neox",
-            span_window=None, rows: Optional[np.ndarray] = None) -> np.ndarray:
+            span_window=None, rows: Optional[np.ndarray] = None, rope_kw: Optional[dict] = None) -> np.ndarray:
     """Prefill output for every query row (or only the rows listed in ``rows``).
 
     q [total_q][Hq][D] holds the unrotated queries of all requests, request-major, in
     the order of ``query_tokens``; the pools must already hold the call's fresh rows.
-    Returns float64 [total_q][Hq][D] (or [len(rows)][Hq][D])."""
+    Returns float64 [total_q][Hq][D] (or [len(rows)][Hq][D]).  ``rope_kw`` passes
+    ``inv_freq`` / ``rotary_dim`` on to ``rope``."""
     q = np.asarray(q)
     D = q.shape[-1]
     scale = _scale(D, softmax_scale)
@@ -235,7 +244,8 @@ def prefill(q, k_pool, v_pool, block_tables, positions, seq_lens, cu_spans, span
             w_tok = span_windows(ss, sf, L, sw)
             pos_row = np.asarray(positions[offs[r]:offs[r] + L], dtype=np.int64)
             o = _attend_request(np.asarray(q[row0 + sel], dtype=np.float64), qi[sel], k_pool, v_pool,
-                                block_tables[r], L, pos_row, w_tok, num_kv_heads, theta, scale, style)
+                                block_tables[r], L, pos_row, w_tok, num_kv_heads, theta, scale, style,
+                                rope_kw=rope_kw)
             out_rows.append((row0 + sel, o))
         row0 += n
     total = row0 if want is None else want.shape[0]
@@ -252,7 +262,7 @@ def prefill(q, k_pool, v_pool, block_tables, positions, seq_lens, cu_spans, span
 
 def decode(q, k_pool, v_pool, block_tables, positions, seq_lens, cu_spans, span_start, span_flags,
            num_kv_heads: int, theta: float, softmax_scale: float = 0.0, style: str = "neox",
-           span_window=None, reqs: Optional[Sequence[int]] = None) -> np.ndarray:
+           span_window=None, reqs: Optional[Sequence[int]] = None, rope_kw: Optional[dict] = None) -> np.ndarray:
     """Decode output: one query per request at its last token n = L_r - 1 (which the
     call's ``kv_write`` has already stored), window taken from that token's span.
     q [R][Hq][D] -> float64 [R][Hq][D] (or only the requests in ``reqs``)."""
@@ -270,7 +280,7 @@ def decode(q, k_pool, v_pool, block_tables, positions, seq_lens, cu_spans, span_
         pos_row = np.asarray(positions[offs[r]:offs[r] + L], dtype=np.int64)
         out[i] = _attend_request(np.asarray(q[r:r + 1], dtype=np.float64), np.array([L - 1]), k_pool,
                                  v_pool, block_tables[r], L, pos_row, w_tok, num_kv_heads, theta,
-                                 scale, style)[0]
+                                 scale, style, rope_kw=rope_kw)[0]
     return out
 
 

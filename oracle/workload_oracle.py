@@ -27,9 +27,10 @@ def run(wl, rows=None, style: str = "neox", pools=None):
     q = wl.q.to(torch.float64).numpy()
     args = (k, v, wl.block_tables, wl.positions, wl.seq_lens, wl.cu_spans, wl.span_start, wl.span_flags,
             wl.num_kv_heads, wl.rope_theta, wl.softmax_scale, style, wl.span_window)
+    rope_kw = {"inv_freq": getattr(wl, "rope_inv_freq", None), "rotary_dim": getattr(wl, "rotary_dim", None)}
     if wl.is_decode:
-        return pic_oracle.decode(q, *args, reqs=rows)
-    return pic_oracle.prefill(q, *args, rows=rows)
+        return pic_oracle.decode(q, *args, reqs=rows, rope_kw=rope_kw)
+    return pic_oracle.prefill(q, *args, rows=rows, rope_kw=rope_kw)
 
 
 def flops(wl) -> float:

@@ -31,7 +31,8 @@ class PicError(RuntimeError):
 class pic_config(ctypes.Structure):
     _fields_ = [("num_q_heads", c_int32), ("num_kv_heads", c_int32), ("head_dim", c_int32),
                 ("block_size", c_int32), ("dtype", c_int32), ("rope_style", c_int32),
-                ("rope_theta", c_double), ("softmax_scale", c_float), ("k_prerotated", c_int32)]
+                ("rope_theta", c_double), ("softmax_scale", c_float), ("k_prerotated", c_int32),
+                ("inv_freq", POINTER(c_double)), ("rotary_dim", c_int32)]
 
 
 class pic_batch_host(ctypes.Structure):
@@ -108,9 +109,15 @@ def lib():
 # ------------------------------------------------------------------------------------
 
 def make_config(num_q_heads, num_kv_heads, head_dim, dtype=PIC_BF16, rope_theta=10000.0,
-                rope_style=PIC_ROPE_NEOX, softmax_scale=0.0, k_prerotated=0, block_size=16) -> pic_config:
-    return pic_config(num_q_heads, num_kv_heads, head_dim, block_size, dtype, rope_style, float(rope_theta),
-                      float(softmax_scale), int(k_prerotated))
+                rope_style=PIC_ROPE_NEOX, softmax_scale=0.0, k_prerotated=0, block_size=16, inv_freq=None,
+                rotary_dim=0) -> pic_config:
+    """A pic_config; ``inv_freq`` (rotary_dim/2 floats) is copied and kept alive with it."""
+    freq = None if inv_freq is None else np.ascontiguousarray(inv_freq, dtype=np.float64)
+    cfg = pic_config(num_q_heads, num_kv_heads, head_dim, block_size, dtype, rope_style, float(rope_theta),
+                     float(softmax_scale), int(k_prerotated),
+                     None if freq is None else freq.ctypes.data_as(POINTER(c_double)), int(rotary_dim or 0))
+    cfg._inv_freq = freq
+    return cfg
 
 
 class HostBatch:

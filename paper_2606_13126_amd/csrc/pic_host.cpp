@@ -40,6 +40,13 @@ pic_status check_config(const pic_config* c) {
     if (!(c->rope_theta > 0.0) || !std::isfinite(c->rope_theta)) return fail(PIC_EINVAL, "rope_theta must be positive");
     if (!(c->softmax_scale >= 0.f) || !std::isfinite(c->softmax_scale)) return fail(PIC_EINVAL, "softmax_scale must be >= 0");
     if (c->k_prerotated != 0 && c->k_prerotated != 1) return fail(PIC_EINVAL, "k_prerotated must be 0 or 1");
+    const int rd = c->rotary_dim ? c->rotary_dim : c->head_dim;
+    if (rd < 2 || rd > c->head_dim || rd % 2) return fail(PIC_EINVAL, "rotary_dim must be 0 or even in [2, head_dim]");
+    if (rd < c->head_dim && c->rope_style != PIC_ROPE_GPTJ)
+        return fail(PIC_EUNSUPPORTED, "partial rotary_dim needs PIC_ROPE_GPTJ");
+    if (c->inv_freq)
+        for (int i = 0; i < rd / 2; ++i)
+            if (!std::isfinite(c->inv_freq[i])) return fail(PIC_EINVAL, "inv_freq must be finite");
     return PIC_OK;
 }
 
@@ -258,11 +265,17 @@ size_t workspace_bytes(const pic_config* c, int64_t n_parts) {
 
 // Phase step of RoPE pair i: omega_i / 2pi revolutions per position as a 64-bit
 // binary fraction, in long double so that the rounding of omega_i stays far below
-// the 2^-64 step.
-void phase_steps(int head_dim, double theta, uint64_t* out) {
+// the 2^-64 step.  omega_i = theta^(-2i/R) or the given inv_freq[i] for i < R/2,
+// nothing past the rotary width.
+void phase_steps(const pic_config* c, uint64_t* out) {
     const long double two_pi = 6.283185307179586476925286766559L;
-    for (int i = 0; i < head_dim / 2; ++i) {
-        long double rev = powl((long double)theta, -2.0L * i / head_dim) / two_pi;
+    const int rd = c->rotary_dim ? c->rotary_dim : c->head_dim;
+    for (int i = 0; i < c->head_dim / 2; ++i) {
+        out[i] = 0;
+        if (i >= rd / 2) continue;
+        const long double om = c->inv_freq ? (long double)c->inv_freq[i]
+                                           : powl((long double)c->rope_theta, -2.0L * i / rd);
+        long double rev = om / two_pi;
         rev -= floorl(rev);
         out[i] = (uint64_t)(rev * 18446744073709551616.0L);
     }
@@ -302,7 +315,7 @@ pic_status run_attention(const pic_config* c, const pic_batch_host* b, const pic
         return fail(PIC_EWORKSPACE, "workspace needs " + std::to_string(need) + " bytes");
 
     pic::Args a{};
-    phase_steps(c->head_dim, c->rope_theta, a.fstep);
+    phase_steps(c, a.fstep);
     a.q = q;
     a.o = o;
     a.k_pool = k_pool;
@@ -314,7 +327,6 @@ pic_status run_attention(const pic_config* c, const pic_batch_host* b, const pic
     a.rope_len = table ? rope->len : 0;
     a.part_o = static_cast<float*>(ws);
     a.part_ml = hp.n_parts ? static_cast<float*>(ws) + (size_t)hp.n_parts * pic::kTileRows * c->head_dim : nullptr;
-    a.theta = c->rope_theta;
     const double scale = c->softmax_scale > 0.f ? (double)c->softmax_scale : 1.0 / std::sqrt((double)c->head_dim);
     a.scale_log2 = (float)(scale * 1.4426950408889634);
     a.max_blocks = dv->max_blocks;
@@ -355,7 +367,9 @@ pic_status pic_rope_table_build(const pic_config* cfg, int32_t num_positions, vo
     if (st) return st;
     if (num_positions < 0) return fail(PIC_EINVAL, "num_positions < 0");
     if (num_positions > 0 && table == nullptr) return fail(PIC_EINVAL, "table is NULL");
-    return hip_status(pic::launch_rope_table(cfg->dtype, cfg->head_dim, cfg->rope_theta, num_positions,
+    pic::RopeSteps steps;
+    phase_steps(cfg, steps.s);
+    return hip_status(pic::launch_rope_table(cfg->dtype, cfg->head_dim, steps, num_positions,
                                              static_cast<float*>(table), stream),
                       "rope table launch");
 }
@@ -368,7 +382,9 @@ pic_status pic_rope_rotate(const pic_config* cfg, const pic_rope_table* rope, vo
     if (n == 0) return PIC_OK;
     if (x == nullptr || positions == nullptr) return fail(PIC_EINVAL, "x and positions must not be NULL");
     const bool table = rope != nullptr && rope->data != nullptr && rope->len > 0;
-    return hip_status(pic::launch_rope_rotate(cfg->dtype, cfg->rope_style, cfg->head_dim, cfg->rope_theta,
+    pic::RopeSteps steps;
+    phase_steps(cfg, steps.s);
+    return hip_status(pic::launch_rope_rotate(cfg->dtype, cfg->rope_style, cfg->head_dim, steps,
                                               table ? static_cast<const float*>(rope->data) : nullptr,
                                               table ? rope->len : 0, x, n, num_heads, positions, stream),
                       "rope rotate launch");

@@ -69,10 +69,14 @@ __host__ __device__ inline int plan_search(const Plan& p, int b) {
     return lo;
 }
 
+// RoPE phase step of pair i as a 64-bit fraction of a revolution per position,
+// round(frac(omega_i / 2pi) * 2^64); 0 for pairs that do not turn
+struct RopeSteps {
+    uint64_t s[64];
+};
+
 struct Args {
-    // RoPE phase step of pair i as a 64-bit fraction of a revolution per position:
-    // round(frac(omega_i / 2pi) * 2^64), omega_i = theta^(-2i/D)
-    uint64_t fstep[64];
+    uint64_t fstep[64];       // RopeSteps of the call
     const void* q;
     void* o;
     const void* k_pool;
@@ -82,7 +86,6 @@ struct Args {
     const float* rope_table;  // [rope_len][D/2] 8-byte entries (format by dtype) or null
     float* part_o;            // [slot][kTileRows][D] unnormalised partial outputs
     float* part_ml;           // [slot][kTileRows][2] running max (log2 units) and sum
-    double theta;
     float scale_log2;         // softmax scale * log2(e)
     int32_t max_blocks;
     int32_t rope_len;
@@ -97,10 +100,10 @@ int32_t host_fail(int32_t st, const char* msg);
 // Launchers implemented in pic_kernels.hip.  Each returns a hipError_t value.
 int launch_kv_write(int dtype, int hkv, int d, void* k_pool, void* v_pool, const void* k_new,
                     const void* v_new, const int32_t* slots, int n, void* stream);
-int launch_rope_table(int dtype, int d, double theta, int n_pos, float* table, void* stream);
+int launch_rope_table(int dtype, int d, const RopeSteps& steps, int n_pos, float* table, void* stream);
 int launch_blocks_copy(int dtype, int hkv, int d, void* k_pool, void* v_pool, void* k_buf, void* v_buf,
                        const int32_t* block_ids, int n, bool to_pool, void* stream);
-int launch_rope_rotate(int dtype, int style, int d, double theta, const float* table, int rope_len, void* x,
+int launch_rope_rotate(int dtype, int style, int d, const RopeSteps& steps, const float* table, int rope_len, void* x,
                        int n, int heads, const int32_t* positions, void* stream);
 int launch_attention(int dtype, int style, int d, bool rope, const Plan& plan, const Args& args, void* stream);
 int launch_decode(int style, int d, bool rope, const Plan& plan, const Args& args, void* stream);

@@ -33,7 +33,6 @@ typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 
 constexpr int kNeox = 0;
 constexpr float kNegBig = -1.0e30f;  // finite "minus infinity" for running maxima
-constexpr double kInv2Pi = 0.15915494309189533577;
 
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
@@ -58,18 +57,13 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
 }
 
 // ---------------------------------------------------------------------------------
-// RoPE angles.  Pair i turns by p * omega_i with omega_i = theta^(-2i/D).  The angle
-// is kept as a 64-bit binary fraction of a revolution, F_i = frac(omega_i / 2pi)
-// scaled by 2^64, so p * F_i (mod 2^64) is the exact phase of any int32 position
-// (negative ones included) up to the rounding of F_i; sin/cos then only see a
-// reduced argument in [-0.5, 0.5) revolutions.
+// RoPE angles.  Pair i turns by p * omega_i.  The angle is kept as a 64-bit binary
+// fraction of a revolution, F_i = frac(omega_i / 2pi) scaled by 2^64 (computed on
+// the host from theta, or from explicit frequencies), so p * F_i (mod 2^64) is the
+// exact phase of any int32 position (negative ones included) up to the rounding of
+// F_i; sin/cos then only see a reduced argument in [-0.5, 0.5) revolutions.  A pair
+// with F_i = 0 (past a partial rotary width) turns by nothing.
 // ---------------------------------------------------------------------------------
-__device__ uint64_t rope_phase_step(double theta, int i, int d) {
-    double rev = pow(theta, -2.0 * (double)i / (double)d) * kInv2Pi;
-    rev -= floor(rev);
-    return (uint64_t)(rev * 18446744073709551616.0);
-}
-
 __device__ __forceinline__ void rope_cs(int32_t pos, uint64_t step, float& c, float& s) {
     const uint64_t ph = (uint64_t)(int64_t)pos * step;
     const float r = (float)(int32_t)(ph >> 32) * 0x1p-32f;
@@ -161,13 +155,13 @@ __global__ void __launch_bounds__(256) blocks_copy_kernel(u32x4_t* __restrict__ 
 // rope_table: entry [p][i] from cos/sin(p * omega_i) in float64, stored as float32
 // (cos, sin) or as bf16 (cos, -sin, sin, cos).
 // ---------------------------------------------------------------------------------
-__global__ void __launch_bounds__(256) rope_table_kernel(uint2* __restrict__ table, int n_pos, int half, int d,
-                                                         double theta, bool bf16_pairs) {
+__global__ void __launch_bounds__(256) rope_table_kernel(uint2* __restrict__ table, int n_pos, int half,
+                                                         RopeSteps steps, bool bf16_pairs) {
     const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (idx >= (int64_t)n_pos * half) return;
     const int p = (int)(idx / half), i = (int)(idx - (int64_t)p * half);
     double c, s;
-    rope_cs_f64(p, rope_phase_step(theta, i, d), c, s);
+    rope_cs_f64(p, steps.s[i], c, s);
     table[idx] = bf16_pairs ? bf16_entry((float)c, (float)s)
                             : make_uint2(__float_as_uint((float)c), __float_as_uint((float)s));
 }
@@ -177,7 +171,7 @@ __global__ void __launch_bounds__(256) rope_table_kernel(uint2* __restrict__ tab
 // ---------------------------------------------------------------------------------
 template <typename T, int STYLE>
 __global__ void __launch_bounds__(256) rope_rotate_kernel(T* __restrict__ x, int64_t n_pairs, int heads, int d,
-                                                          double theta, const int32_t* __restrict__ positions,
+                                                          RopeSteps steps, const int32_t* __restrict__ positions,
                                                           const uint2* __restrict__ table, int rope_len) {
     const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (idx >= n_pairs) return;
@@ -195,7 +189,7 @@ __global__ void __launch_bounds__(256) rope_rotate_kernel(T* __restrict__ x, int
             cs_from_bf16_entry(v, c, s);
         }
     } else {
-        rope_cs(pos, rope_phase_step(theta, i, d), c, s);
+        rope_cs(pos, steps.s[i], c, s);
     }
     T* row = x + rh * d;
     const int ia = STYLE == kNeox ? i : 2 * i, ib = STYLE == kNeox ? i + half : 2 * i + 1;
@@ -1433,15 +1427,15 @@ int launch_blocks_copy(int dtype, int hkv, int d, void* k_pool, void* v_pool, vo
     return hipGetLastError();
 }
 
-int launch_rope_table(int dtype, int d, double theta, int n_pos, float* table, void* stream) {
+int launch_rope_table(int dtype, int d, const RopeSteps& steps, int n_pos, float* table, void* stream) {
     const int64_t n = (int64_t)n_pos * (d / 2);
     if (n == 0) return hipSuccess;
     hipLaunchKernelGGL(rope_table_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, (hipStream_t)stream,
-                       reinterpret_cast<uint2*>(table), n_pos, d / 2, d, theta, dtype != 1);
+                       reinterpret_cast<uint2*>(table), n_pos, d / 2, steps, dtype != 1);
     return hipGetLastError();
 }
 
-int launch_rope_rotate(int dtype, int style, int d, double theta, const float* table, int rope_len, void* x, int n,
+int launch_rope_rotate(int dtype, int style, int d, const RopeSteps& steps, const float* table, int rope_len, void* x, int n,
                        int heads, const int32_t* positions, void* stream) {
     const int64_t n_pairs = (int64_t)n * heads * (d / 2);
     if (n_pairs == 0) return hipSuccess;
@@ -1451,17 +1445,17 @@ int launch_rope_rotate(int dtype, int style, int d, double theta, const float* t
     if (dtype == 1) {
         if (style == kNeox)
             hipLaunchKernelGGL((rope_rotate_kernel<float, 0>), grid, dim3(256), 0, st, static_cast<float*>(x),
-                               n_pairs, heads, d, theta, positions, t, rope_len);
+                               n_pairs, heads, d, steps, positions, t, rope_len);
         else
             hipLaunchKernelGGL((rope_rotate_kernel<float, 1>), grid, dim3(256), 0, st, static_cast<float*>(x),
-                               n_pairs, heads, d, theta, positions, t, rope_len);
+                               n_pairs, heads, d, steps, positions, t, rope_len);
     } else {
         if (style == kNeox)
             hipLaunchKernelGGL((rope_rotate_kernel<__bf16, 0>), grid, dim3(256), 0, st, static_cast<__bf16*>(x),
-                               n_pairs, heads, d, theta, positions, t, rope_len);
+                               n_pairs, heads, d, steps, positions, t, rope_len);
         else
             hipLaunchKernelGGL((rope_rotate_kernel<__bf16, 1>), grid, dim3(256), 0, st, static_cast<__bf16*>(x),
-                               n_pairs, heads, d, theta, positions, t, rope_len);
+                               n_pairs, heads, d, steps, positions, t, rope_len);
     }
     return hipGetLastError();
 }

@@ -16,7 +16,8 @@ from . import _binding as B
 def config_of(wl, k_prerotated: bool = False, rope_style: int = B.PIC_ROPE_NEOX):
     dtype = B.PIC_F32 if wl.dtype == torch.float32 else B.PIC_BF16
     return B.make_config(wl.num_q_heads, wl.num_kv_heads, wl.head_dim, dtype=dtype, rope_theta=wl.rope_theta,
-                         rope_style=rope_style, softmax_scale=wl.softmax_scale, k_prerotated=int(k_prerotated))
+                         rope_style=rope_style, softmax_scale=wl.softmax_scale, k_prerotated=int(k_prerotated),
+                         inv_freq=getattr(wl, "rope_inv_freq", None), rotary_dim=getattr(wl, "rotary_dim", None))
 
 
 class DeviceBatch:

@@ -41,3 +41,32 @@ def windows_decode_case():
                       value_scale=0.5, decode=True)
     wl.span_window = np.array([-1, -1, -1, 64, -1, -1, 48, 37], dtype=np.int32)
     return wl
+
+
+def llama3_inv_freq(head_dim, theta, factor=8.0, low_freq_factor=1.0, high_freq_factor=4.0, original_max=8192):
+    """Band-scaled RoPE frequencies of the Llama 3.1 family: wavelengths shorter than
+    original_max / high_freq_factor keep their frequency, longer than
+    original_max / low_freq_factor are slowed by ``factor``, and the band between
+    interpolates linearly in original_max / wavelength."""
+    om = 1.0 / np.power(float(theta), np.arange(0, head_dim, 2, dtype=np.float64) / head_dim)
+    wavelen = 2.0 * np.pi / om
+    smooth = (original_max / wavelen - low_freq_factor) / (high_freq_factor - low_freq_factor)
+    mid = (1.0 - smooth) * om / factor + smooth * om
+    out = np.where(wavelen < original_max / high_freq_factor, om,
+                   np.where(wavelen > original_max / low_freq_factor, om / factor, mid))
+    return out
+
+
+def rope_variant_case(dtype, D=128, rotary_dim=None, inv_freq=None, decode=False, seed=51):
+    """Prefill (or decode) batch with long positions for the RoPE-variant tests."""
+    if decode:
+        reqs = [[Sp(64, S, key="a"), Sp(300, S), Sp(1, Pd, fresh=True)],
+                [Sp(48, S, key="b"), Sp(64, S, key="a"), Sp(1, 0, fresh=True)]]
+    else:
+        reqs = [[Sp(64, S, key="a"), Sp(200, S | Q, fresh=True), Sp(45, Pd | Q, fresh=True)],
+                [Sp(48, S, key="b"), Sp(64, S, key="a"), Sp(33, Pd | Q, fresh=True)]]
+    wl = W.small_case(f"rope_variant_d{D}_r{rotary_dim}", reqs, Hq=8, Hkv=2, D=D, theta=5e5, dtype=dtype,
+                      seed=seed, value_scale=0.5, decode=decode, position_offsets=[60000, 123])
+    wl.rotary_dim = rotary_dim
+    wl.rope_inv_freq = inv_freq
+    return wl

@@ -115,6 +115,70 @@ def test_rope_closed_form_first_pair():
     assert y[D - 1] == pytest.approx(math.sin(ang), abs=1e-13)
 
 
+# ---- RoPE variants: explicit frequencies and partial rotary width ------------------
+
+def test_rope_default_frequencies_through_override():
+    x = RNG.standard_normal((5, 3, 64))
+    pos = RNG.integers(-5000, 5000, size=(5, 3))
+    assert np.array_equal(O.rope(x, pos, 5e5), O.rope(x, pos, 5e5, inv_freq=O.rope_inv_freq(64, 5e5)))
+
+
+@pytest.mark.parametrize("style", ["neox", "gptj"])
+def test_rope_scaled_frequencies_are_scaled_positions(style):
+    # frequencies c * omega turn position p as far as the plain frequencies turn c * p
+    # (position interpolation with c = 1/4 is the same statement read backwards)
+    x = RNG.standard_normal((7, 128))
+    pos = RNG.integers(0, 9000, size=7)
+    om = O.rope_inv_freq(128, 1e4)
+    assert np.allclose(O.rope(x, pos, 1e4, style, inv_freq=3.0 * om), O.rope(x, 3 * pos, 1e4, style), atol=1e-9)
+    assert np.allclose(O.rope(x, 4 * pos, 1e4, style, inv_freq=om / 4.0), O.rope(x, pos, 1e4, style), atol=1e-9)
+
+
+def test_rope_partial_gptj_closed_form():
+    # R = 4 of D = 10: pairs (0,1) at omega_0 = 1 and (2,3) at theta^(-1/2); 4..9 pass
+    x = RNG.standard_normal(10)
+    p, theta = 7, 100.0
+    y = O.rope(x, np.array(p), theta, "gptj", rotary_dim=4)
+    for (a, b), om in (((0, 1), 1.0), ((2, 3), theta ** -0.5)):
+        c, s = math.cos(p * om), math.sin(p * om)
+        assert abs(y[a] - (x[a] * c - x[b] * s)) < 1e-13 and abs(y[b] - (x[b] * c + x[a] * s)) < 1e-13
+    assert np.array_equal(y[4:], x[4:])
+
+
+def test_rope_partial_neox_closed_form():
+    # R = 4 of D = 10, NeoX: element i pairs with i + R/2, so (0,2) and (1,3)
+    x = RNG.standard_normal(10)
+    p, theta = 5, 100.0
+    y = O.rope(x, np.array(p), theta, "neox", rotary_dim=4)
+    for (a, b), om in (((0, 2), 1.0), ((1, 3), theta ** -0.5)):
+        c, s = math.cos(p * om), math.sin(p * om)
+        assert abs(y[a] - (x[a] * c - x[b] * s)) < 1e-13 and abs(y[b] - (x[b] * c + x[a] * s)) < 1e-13
+    assert np.array_equal(y[4:], x[4:])
+
+
+@pytest.mark.parametrize("style", ["neox", "gptj"])
+def test_rope_partial_is_full_rope_of_the_prefix(style):
+    x = RNG.standard_normal((6, 64))
+    pos = RNG.integers(0, 4000, size=6)
+    y = O.rope(x, pos, 1e4, style, rotary_dim=32)
+    assert np.allclose(y[:, :32], O.rope(x[:, :32], pos, 1e4, style), atol=1e-12)
+    assert np.array_equal(y[:, 32:], x[:, 32:])
+
+
+def test_variant_attention_is_shift_invariant():
+    # any frequencies and a partial width keep scores relative: a shifted request
+    # attends the same way
+    wl = W.config0()
+    wl.rotary_dim = 48
+    wl.rope_inv_freq = np.linspace(1.0, 1e-3, 24) * 0.9
+    o0 = WO.run(wl, style="gptj")
+    wl.positions = wl.positions + np.int32(4321)
+    assert np.max(np.abs(o0 - WO.run(wl, style="gptj"))) <= 1e-9
+    # and it is not the plain rotation
+    wl.rotary_dim, wl.rope_inv_freq = None, None
+    assert np.max(np.abs(o0 - WO.run(wl, style="gptj"))) > 1e-3
+
+
 def test_rope_relative():
     # (R_a q)^T (R_b k) depends on a - b only
     q, k = RNG.standard_normal(32), RNG.standard_normal(32)
@@ -355,14 +419,14 @@ def test_span_windows_rule():
 # ---- planted mistakes: the pins above must catch each of them ------------------------
 
 def _mut_sign(orig):
-    def f(x, pos, theta, style="neox"):
-        return orig(x, -np.asarray(pos), theta, style)
+    def f(x, pos, theta, style="neox", **kw):
+        return orig(x, -np.asarray(pos), theta, style, **kw)
     return f
 
 
 def _mut_pairing(orig):
-    def f(x, pos, theta, style="neox"):
-        return orig(x, pos, theta, "gptj" if style == "neox" else "neox")
+    def f(x, pos, theta, style="neox", **kw):
+        return orig(x, pos, theta, "gptj" if style == "neox" else "neox", **kw)
     return f
 
 

@@ -71,6 +71,8 @@ class Workload:
     block_size: int = BLOCK
     softmax_scale: float = 0.0  # 0 means 1/sqrt(head_dim)
     span_window: Optional[np.ndarray] = None  # optional explicit window start per span
+    rope_inv_freq: Optional[np.ndarray] = None  # optional RoPE frequencies [rotary_dim/2]
+    rotary_dim: Optional[int] = None            # optional partial rotary width (None: head_dim)
     info: dict = field(default_factory=dict)
 
     @property
