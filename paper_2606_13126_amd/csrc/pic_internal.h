@@ -84,7 +84,9 @@ struct Args {
     const int32_t* block_tables;
     const int32_t* positions;
     const float* rope_table;  // [rope_len][D/2] 8-byte entries (format by dtype) or null
-    float* part_o;            // [slot][kTileRows][D] unnormalised partial outputs
+    float* part_o;            // [slot][kTileRows][D] split partial outputs: prefill stores
+                              // them normalised by the split's sum as bf16, decode
+                              // unnormalised as fp32
     float* part_ml;           // [slot][kTileRows][2] running max (log2 units) and sum
     float scale_log2;         // softmax scale * log2(e)
     int32_t max_blocks;

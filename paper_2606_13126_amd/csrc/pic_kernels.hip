@@ -727,15 +727,19 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
                 *reinterpret_cast<u32x2_t*>(op + d) = w;
             }
     } else {
+        // the split's output normalised by its own sum, in bf16 (half the partial
+        // traffic of fp32), with the split's running maximum and sum beside it
         const size_t slot = (size_t)part_base + (size_t)cluster * g.n_rt + rt;
-        float* po = a.part_o + (slot * kTileRows + (row - row_lo)) * D;
+        uint16_t* po = reinterpret_cast<uint16_t*>(a.part_o) + (slot * kTileRows + (row - row_lo)) * D;
+        const float inv = lt > 0.f ? 1.f / lt : 0.f;
 #pragma unroll
         for (int db = 0; db < DB; ++db)
 #pragma unroll
             for (int q4 = 0; q4 < 4; ++q4) {
                 const int d = db * 32 + 8 * q4 + 4 * hi;
-                *reinterpret_cast<float4*>(po + d) =
-                    make_float4(acc[db][4 * q4], acc[db][4 * q4 + 1], acc[db][4 * q4 + 2], acc[db][4 * q4 + 3]);
+                const u32x2_t w = {pack_bf16(acc[db][4 * q4] * inv, acc[db][4 * q4 + 1] * inv),
+                                   pack_bf16(acc[db][4 * q4 + 2] * inv, acc[db][4 * q4 + 3] * inv)};
+                *reinterpret_cast<u32x2_t*>(po + d) = w;
             }
         if (hi == 0)
             *reinterpret_cast<float2*>(a.part_ml + (slot * kTileRows + (row - row_lo)) * 2) = make_float2(m_run, lt);
@@ -775,29 +779,32 @@ __global__ void __launch_bounds__(kMergeRows * D / 4) merge_kernel(const Plan pl
     const size_t slot0 = (size_t)part_base + (size_t)kvh * g.n_split * g.n_rt + rt;
     float M = kNegBig, den = 0.f;
     float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
+    const uint16_t* part = reinterpret_cast<const uint16_t*>(a.part_o);
     for (int s0 = 0; s0 < n_live; s0 += U) {
         float2 ml[U];
-        float4 v[U];
+        u32x2_t v[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             ml[u] = make_float2(kNegBig, 0.f);
-            v[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+            v[u] = u32x2_t{0, 0};
             if (s0 + u < n_live) {
                 const size_t slot = slot0 + (size_t)(s0 + u) * g.n_rt;
                 ml[u] = *reinterpret_cast<const float2*>(a.part_ml + (slot * kTileRows + r) * 2);
-                v[u] = *reinterpret_cast<const float4*>(a.part_o + (slot * kTileRows + r) * D + q4 * 4);
+                v[u] = *reinterpret_cast<const u32x2_t*>(part + (slot * kTileRows + r) * D + q4 * 4);
             }
         }
+        // each split's output is normalised: weight it by its sum times 2^(m_s - M)
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             if (!(ml[u].y > 0.f)) continue;   // split saw no key of this row
             const float m_new = fmaxf(M, ml[u].x);
-            const float c_old = __builtin_amdgcn_exp2f(M - m_new), c_new = __builtin_amdgcn_exp2f(ml[u].x - m_new);
-            num.x = num.x * c_old + c_new * v[u].x;
-            num.y = num.y * c_old + c_new * v[u].y;
-            num.z = num.z * c_old + c_new * v[u].z;
-            num.w = num.w * c_old + c_new * v[u].w;
-            den = den * c_old + c_new * ml[u].y;
+            const float c_old = __builtin_amdgcn_exp2f(M - m_new);
+            const float w = __builtin_amdgcn_exp2f(ml[u].x - m_new) * ml[u].y;
+            num.x = num.x * c_old + w * bf_lo(v[u][0]);
+            num.y = num.y * c_old + w * bf_hi(v[u][0]);
+            num.z = num.z * c_old + w * bf_lo(v[u][1]);
+            num.w = num.w * c_old + w * bf_hi(v[u][1]);
+            den = den * c_old + w;
             M = m_new;
         }
     }
