@@ -76,8 +76,9 @@ typedef struct pic_config {
                                  baseline FlashAttention of Sec. 3.2.2, for comparison) */
     /* RoPE variants of the models the method applies to (Sec. 3.2.1 takes the model's
      * own rotary embedding).  rotary_dim R: only the first R elements of q and k turn
-     * (partial rotary), 0 means R = D; even, 2 <= R <= D, and R < D only with
-     * PIC_ROPE_GPTJ (pairs 2i, 2i+1 for i < R/2).  inv_freq: HOST [R/2] frequencies
+     * (partial rotary), 0 means R = D; even, 2 <= R <= D.  Within them PIC_ROPE_GPTJ
+     * pairs 2i with 2i+1 and PIC_ROPE_NEOX pairs i with i + R/2 (NeoX with R < D
+     * needs R % 16 == 0, else PIC_EUNSUPPORTED).  inv_freq: HOST [R/2] frequencies
      * omega_i (radians per position), finite, read during each call that takes cfg --
      * scaled-RoPE variants (position interpolation, NTK, Llama-3-style band scaling)
      * change only these; NULL means omega_i = theta^(-2i/R). */

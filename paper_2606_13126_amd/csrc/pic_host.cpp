@@ -42,8 +42,8 @@ pic_status check_config(const pic_config* c) {
     if (c->k_prerotated != 0 && c->k_prerotated != 1) return fail(PIC_EINVAL, "k_prerotated must be 0 or 1");
     const int rd = c->rotary_dim ? c->rotary_dim : c->head_dim;
     if (rd < 2 || rd > c->head_dim || rd % 2) return fail(PIC_EINVAL, "rotary_dim must be 0 or even in [2, head_dim]");
-    if (rd < c->head_dim && c->rope_style != PIC_ROPE_GPTJ)
-        return fail(PIC_EUNSUPPORTED, "partial rotary_dim needs PIC_ROPE_GPTJ");
+    if (rd < c->head_dim && c->rope_style == PIC_ROPE_NEOX && rd % 16 != 0)
+        return fail(PIC_EUNSUPPORTED, "partial rotary_dim with NeoX pairing must be a multiple of 16");
     if (c->inv_freq)
         for (int i = 0; i < rd / 2; ++i)
             if (!std::isfinite(c->inv_freq[i])) return fail(PIC_EINVAL, "inv_freq must be finite");
@@ -281,6 +281,32 @@ void phase_steps(const pic_config* c, uint64_t* out) {
     }
 }
 
+// Kernel-layout chunk c of q and K (8 elements) -> model chunk, 4 bits per chunk.
+// NeoX with rotary width R < D: kernel chunks [0, R/16) and [D/16, D/16 + R/16) are
+// the model's two rotary halves, the other kernel chunks the model's pass-through
+// chunks [R/8, D/8) in order.
+uint64_t chunk_map(const pic_config* c) {
+    const int ch = c->head_dim / 8, rd = c->rotary_dim ? c->rotary_dim : c->head_dim;
+    int map[16];
+    for (int i = 0; i < ch; ++i) map[i] = i;
+    if (c->rope_style == PIC_ROPE_NEOX && rd < c->head_dim && !c->k_prerotated) {
+        const int rc = rd / 16;
+        int next = 2 * rc;
+        for (int i = 0; i < ch / 2; ++i) {
+            if (i < rc) {
+                map[i] = i;
+                map[i + ch / 2] = rc + i;
+            } else {
+                map[i] = next++;
+                map[i + ch / 2] = next++;
+            }
+        }
+    }
+    uint64_t m = 0;
+    for (int i = 0; i < ch; ++i) m |= (uint64_t)map[i] << (4 * i);
+    return m;
+}
+
 pic_status hip_status(int e, const char* what) {
     if (e != hipSuccess) return fail(PIC_EHIP, std::string(what) + ": " + hipGetErrorString((hipError_t)e));
     return PIC_OK;
@@ -316,6 +342,7 @@ pic_status run_attention(const pic_config* c, const pic_batch_host* b, const pic
 
     pic::Args a{};
     phase_steps(c, a.fstep);
+    a.chunk_map = chunk_map(c);
     a.q = q;
     a.o = o;
     a.k_pool = k_pool;
@@ -384,7 +411,8 @@ pic_status pic_rope_rotate(const pic_config* cfg, const pic_rope_table* rope, vo
     const bool table = rope != nullptr && rope->data != nullptr && rope->len > 0;
     pic::RopeSteps steps;
     phase_steps(cfg, steps.s);
-    return hip_status(pic::launch_rope_rotate(cfg->dtype, cfg->rope_style, cfg->head_dim, steps,
+    const int rot_half = (cfg->rotary_dim ? cfg->rotary_dim : cfg->head_dim) / 2;
+    return hip_status(pic::launch_rope_rotate(cfg->dtype, cfg->rope_style, cfg->head_dim, rot_half, steps,
                                               table ? static_cast<const float*>(rope->data) : nullptr,
                                               table ? rope->len : 0, x, n, num_heads, positions, stream),
                       "rope rotate launch");

@@ -77,6 +77,11 @@ struct RopeSteps {
 
 struct Args {
     uint64_t fstep[64];       // RopeSteps of the call
+    // q and K are read in "kernel layout": its 8-element chunk c is the model's chunk
+    // (chunk_map >> 4c) & 15.  Identity except for NeoX pairing with a partial rotary
+    // width R, where kernel pair (i, i + D/2) must be the model pair (i, i + R/2) for
+    // i < R/2 and a pass-through pair (step 0) otherwise.
+    uint64_t chunk_map;
     const void* q;
     void* o;
     const void* k_pool;
@@ -105,7 +110,7 @@ int launch_kv_write(int dtype, int hkv, int d, void* k_pool, void* v_pool, const
 int launch_rope_table(int dtype, int d, const RopeSteps& steps, int n_pos, float* table, void* stream);
 int launch_blocks_copy(int dtype, int hkv, int d, void* k_pool, void* v_pool, void* k_buf, void* v_buf,
                        const int32_t* block_ids, int n, bool to_pool, void* stream);
-int launch_rope_rotate(int dtype, int style, int d, const RopeSteps& steps, const float* table, int rope_len, void* x,
+int launch_rope_rotate(int dtype, int style, int d, int rot_half, const RopeSteps& steps, const float* table, int rope_len, void* x,
                        int n, int heads, const int32_t* positions, void* stream);
 int launch_attention(int dtype, int style, int d, bool rope, const Plan& plan, const Args& args, void* stream);
 int launch_decode(int style, int d, bool rope, const Plan& plan, const Args& args, void* stream);

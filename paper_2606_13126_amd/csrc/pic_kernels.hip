@@ -76,6 +76,9 @@ __device__ __forceinline__ void rope_cs_f64(int32_t pos, uint64_t step, double& 
     sincospi(2.0 * r, &s, &c);
 }
 
+// Model chunk (8 elements) read into kernel-layout chunk c of q or K.
+__device__ __forceinline__ int model_chunk(uint64_t map, int c) { return (int)((map >> (4 * c)) & 15); }
+
 // Table entries: float32 kernels read (cos, sin) as two floats; bf16 kernels read
 // (cos, -sin) and (sin, cos) as two bf16 pairs, so that rotating a pair (x, y) is
 // two 2-element dot products: x' = (x, y).(c, -s), y' = (x, y).(s, c).
@@ -171,13 +174,15 @@ __global__ void __launch_bounds__(256) rope_table_kernel(uint2* __restrict__ tab
 // ---------------------------------------------------------------------------------
 template <typename T, int STYLE>
 __global__ void __launch_bounds__(256) rope_rotate_kernel(T* __restrict__ x, int64_t n_pairs, int heads, int d,
-                                                          RopeSteps steps, const int32_t* __restrict__ positions,
+                                                          int rot_half, RopeSteps steps,
+                                                          const int32_t* __restrict__ positions,
                                                           const uint2* __restrict__ table, int rope_len) {
     const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (idx >= n_pairs) return;
     const int half = d / 2;
     const int64_t rh = idx / half;                 // row * heads + h
     const int i = (int)(idx - rh * half);
+    if (i >= rot_half) return;                     // past the rotary width: unchanged
     const int32_t pos = positions[rh / heads];
     float c, s;
     if (table != nullptr && (uint32_t)pos < (uint32_t)rope_len) {
@@ -192,7 +197,7 @@ __global__ void __launch_bounds__(256) rope_rotate_kernel(T* __restrict__ x, int
         rope_cs(pos, steps.s[i], c, s);
     }
     T* row = x + rh * d;
-    const int ia = STYLE == kNeox ? i : 2 * i, ib = STYLE == kNeox ? i + half : 2 * i + 1;
+    const int ia = STYLE == kNeox ? i : 2 * i, ib = STYLE == kNeox ? i + rot_half : 2 * i + 1;
     const float a = (float)row[ia], b = (float)row[ib];
     row[ia] = (T)(a * c - b * s);
     row[ib] = (T)(b * c + a * s);
@@ -376,7 +381,8 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
                              ((size_t)(g.q_row0 + toff) * a.hq + (size_t)kvh * G + hl) * D;
 #pragma unroll
         for (int kd = 0; kd < KD; ++kd)
-            qraw[kd] = row_valid ? *reinterpret_cast<const u32x4_t*>(qp + kd * 16 + 8 * hi) : u32x4_t{0, 0, 0, 0};
+            qraw[kd] = row_valid ? *reinterpret_cast<const u32x4_t*>(qp + model_chunk(a.chunk_map, 2 * kd + hi) * 8)
+                                 : u32x4_t{0, 0, 0, 0};
         if (ROPE && row_valid) qpos = a.positions[g.pos_off + g.tok0 + toff];
     };
     auto q_finish = [&]() {   // rotate, scale by softmax_scale*log2(e), round to bf16
@@ -499,8 +505,8 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
             const int phys = mblk[t & 1][kr >> 4];
             const uint16_t* kp = kpool + (((size_t)phys * a.hkv + kvh) * kBlock + (j & 15)) * D;
             if (STYLE == kNeox) {
-                r.k[0] = *reinterpret_cast<const u32x4_t*>(kp + sc * 8);
-                r.k[1] = *reinterpret_cast<const u32x4_t*>(kp + HALF + sc * 8);
+                r.k[0] = *reinterpret_cast<const u32x4_t*>(kp + model_chunk(a.chunk_map, sc) * 8);
+                r.k[1] = *reinterpret_cast<const u32x4_t*>(kp + model_chunk(a.chunk_map, sc + CH / 2) * 8);
             } else {
                 r.k[0] = *reinterpret_cast<const u32x4_t*>(kp + sc * 16);
                 r.k[1] = *reinterpret_cast<const u32x4_t*>(kp + sc * 16 + 8);
@@ -977,7 +983,8 @@ __global__ void __launch_bounds__(dec_heads(D) * 64, 1) decode_bf16(const Plan p
         float xf[KD][8];
 #pragma unroll
         for (int kd = 0; kd < KD; ++kd) {
-            const u32x4_t raw = qv ? *reinterpret_cast<const u32x4_t*>(qp + kd * 32 + 8 * q4) : u32x4_t{0, 0, 0, 0};
+            const u32x4_t raw =
+                qv ? *reinterpret_cast<const u32x4_t*>(qp + model_chunk(a.chunk_map, kd * 4 + q4) * 8) : u32x4_t{0, 0, 0, 0};
 #pragma unroll
             for (int m = 0; m < 4; ++m) {
                 xf[kd][2 * m] = bf_lo(raw[m]);
@@ -1088,7 +1095,8 @@ __global__ void __launch_bounds__(dec_heads(D) * 64, 1) decode_bf16(const Plan p
     // 16*db + 4*(lane%4))
     int k_off[KD];
 #pragma unroll
-    for (int kd = 0; kd < KD; ++kd) k_off[kd] = wave * HSZ + c16 * D + (((kd * 4 + q4) ^ swz<D>(c16)) << 3);
+    for (int kd = 0; kd < KD; ++kd)
+        k_off[kd] = wave * HSZ + c16 * D + ((model_chunk(a.chunk_map, kd * 4 + q4) ^ swz<D>(c16)) << 3);
     constexpr int NTC = STYLE == kNeox ? 4 * (KD / 2) : 2 * KD;
     int t_off[NTC];
 #pragma unroll
@@ -1325,10 +1333,17 @@ __global__ void __launch_bounds__(64) attn_f32(const Plan plan, const Args a) {
     };
 
     const float* qp = static_cast<const float*>(a.q) + ((size_t)(g.q_row0 + toff) * a.hq + h) * D;
+    // element e of this lane holds kernel-layout dimension lane + 64 e of q and K
+    int me[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const int d = lane + 64 * e;
+        me[e] = model_chunk(a.chunk_map, d >> 3) * 8 + (d & 7);
+    }
     float q[E], o[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) {
-        q[e] = qp[lane + 64 * e];
+        q[e] = qp[me[e]];
         o[e] = 0.f;
     }
     if (ROPE) rotate(q, a.positions[g.pos_off + t]);
@@ -1344,7 +1359,7 @@ __global__ void __launch_bounds__(64) attn_f32(const Plan plan, const Args a) {
         float k[E], v[E];
 #pragma unroll
         for (int e = 0; e < E; ++e) {
-            k[e] = kpool[base + lane + 64 * e];
+            k[e] = kpool[base + me[e]];
             v[e] = vpool[base + lane + 64 * e];
         }
         if (ROPE) rotate(k, a.positions[g.pos_off + j]);
@@ -1442,7 +1457,7 @@ int launch_rope_table(int dtype, int d, const RopeSteps& steps, int n_pos, float
     return hipGetLastError();
 }
 
-int launch_rope_rotate(int dtype, int style, int d, const RopeSteps& steps, const float* table, int rope_len, void* x, int n,
+int launch_rope_rotate(int dtype, int style, int d, int rot_half, const RopeSteps& steps, const float* table, int rope_len, void* x, int n,
                        int heads, const int32_t* positions, void* stream) {
     const int64_t n_pairs = (int64_t)n * heads * (d / 2);
     if (n_pairs == 0) return hipSuccess;
@@ -1452,17 +1467,17 @@ int launch_rope_rotate(int dtype, int style, int d, const RopeSteps& steps, cons
     if (dtype == 1) {
         if (style == kNeox)
             hipLaunchKernelGGL((rope_rotate_kernel<float, 0>), grid, dim3(256), 0, st, static_cast<float*>(x),
-                               n_pairs, heads, d, steps, positions, t, rope_len);
+                               n_pairs, heads, d, rot_half, steps, positions, t, rope_len);
         else
             hipLaunchKernelGGL((rope_rotate_kernel<float, 1>), grid, dim3(256), 0, st, static_cast<float*>(x),
-                               n_pairs, heads, d, steps, positions, t, rope_len);
+                               n_pairs, heads, d, rot_half, steps, positions, t, rope_len);
     } else {
         if (style == kNeox)
             hipLaunchKernelGGL((rope_rotate_kernel<__bf16, 0>), grid, dim3(256), 0, st, static_cast<__bf16*>(x),
-                               n_pairs, heads, d, steps, positions, t, rope_len);
+                               n_pairs, heads, d, rot_half, steps, positions, t, rope_len);
         else
             hipLaunchKernelGGL((rope_rotate_kernel<__bf16, 1>), grid, dim3(256), 0, st, static_cast<__bf16*>(x),
-                               n_pairs, heads, d, steps, positions, t, rope_len);
+                               n_pairs, heads, d, rot_half, steps, positions, t, rope_len);
     }
     return hipGetLastError();
 }

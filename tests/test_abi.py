@@ -55,7 +55,7 @@ def batch_of(wl):
     (dict(num_q_heads=4, num_kv_heads=1, head_dim=64, rope_style=5), B.PIC_EINVAL),
     (dict(num_q_heads=4, num_kv_heads=1, head_dim=64, rotary_dim=33, rope_style=1), B.PIC_EINVAL),
     (dict(num_q_heads=4, num_kv_heads=1, head_dim=64, rotary_dim=66, rope_style=1), B.PIC_EINVAL),
-    (dict(num_q_heads=4, num_kv_heads=1, head_dim=64, rotary_dim=32), B.PIC_EUNSUPPORTED),
+    (dict(num_q_heads=4, num_kv_heads=1, head_dim=64, rotary_dim=24), B.PIC_EUNSUPPORTED),
     (dict(num_q_heads=4, num_kv_heads=1, head_dim=64, inv_freq=[1.0] * 31 + [float("nan")]), B.PIC_EINVAL),
     (dict(num_q_heads=4, num_kv_heads=1, head_dim=64, rotary_dim=16, rope_style=1,
           inv_freq=[0.5] * 7 + [float("inf")]), B.PIC_EINVAL),

@@ -43,12 +43,24 @@ def test_partial_rotary_gptj_prefill(D, R, dtype):
     run_check(rope_variant_case(dtype, D=D, rotary_dim=R), 1, True)
 
 
+@pytest.mark.parametrize("D,R", [(128, 32), (128, 96), (64, 16), (64, 48), (128, 16)])
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_partial_rotary_neox_prefill(D, R, dtype):
+    run_check(rope_variant_case(dtype, D=D, rotary_dim=R), 0, True)
+
+
+def test_partial_rotary_neox_computed_cossin_decode():
+    freq = llama3_inv_freq(32, 1e4)
+    run_check(rope_variant_case(torch.bfloat16, rotary_dim=32, inv_freq=freq, decode=True), 0, False)
+    run_check(rope_variant_case(torch.bfloat16, rotary_dim=64, decode=True), 0, True)
+
+
 def test_partial_rotary_with_scaled_frequencies_computed_cossin():
     wl = rope_variant_case(torch.bfloat16, rotary_dim=64, inv_freq=llama3_inv_freq(64, 1e4) * 1.7)
     run_check(wl, 1, False)
 
 
-@pytest.mark.parametrize("style,R,table", [(0, None, True), (1, 64, True), (1, 96, False)])
+@pytest.mark.parametrize("style,R,table", [(0, None, True), (1, 64, True), (1, 96, False), (0, 64, True)])
 def test_variants_decode(style, R, table):
     freq = llama3_inv_freq(R or 128, 5e5)
     run_check(rope_variant_case(torch.bfloat16, rotary_dim=R, inv_freq=freq, decode=True), style, table)
@@ -70,7 +82,8 @@ def test_variant_table_entries():
     assert (got[:, R // 2:, 0] == 1.0).all() and (got[:, R // 2:, 1] == 0.0).all()
 
 
-def test_variant_prerotated_equals_fused():
+@pytest.mark.parametrize("style", [0, 1])
+def test_variant_prerotated_equals_fused(style):
     # the conventional rotation (pic_rope_rotate) with the same variant, applied to
     # every stored key and to the queries, gives the fused result
     import paper_2606_13126_amd as P
@@ -80,8 +93,8 @@ def test_variant_prerotated_equals_fused():
                       Hq=8, Hkv=2, D=128, theta=5e5, dtype=torch.bfloat16, seed=52, value_scale=0.5,
                       position_offsets=[60000])
     wl.rotary_dim, wl.rope_inv_freq = 96, llama3_inv_freq(96, 5e5)
-    fused = gpu_run(wl, rope_style=1)
-    ctl = DeviceBatch(wl, k_prerotated=True, rope_style=1, table_positions=int(wl.positions.max()) + 1)
+    fused = gpu_run(wl, rope_style=style)
+    ctl = DeviceBatch(wl, k_prerotated=True, rope_style=style, table_positions=int(wl.positions.max()) + 1)
     ctl.write()
     # one request: rotate every stored key once, at its position
     kp = ctl.k_pool.permute(0, 2, 1, 3).reshape(-1, wl.num_kv_heads, wl.head_dim)
@@ -99,4 +112,4 @@ def test_variant_prerotated_equals_fused():
     ctl.attend()
     torch.cuda.synchronize()
     assert_close(to_np(ctl.o), to_np(fused.o), wl.dtype, "pre-rotated variant vs fused")
-    assert_close(to_np(fused.o), WO.run(wl, style="gptj"), wl.dtype, "fused variant vs oracle")
+    assert_close(to_np(fused.o), WO.run(wl, style="gptj" if style else "neox"), wl.dtype, "fused variant vs oracle")
