@@ -147,7 +147,8 @@ pic_status pic_rope_rotate(const pic_config* cfg, const pic_rope_table* rope, vo
  * unrotated).  Row i of k_new/v_new (DEVICE [n][Hkv][D]) goes to slot
  * s = slot_mapping[i] (DEVICE [n]): pool[s/16][h][s%16][:] for every KV head h,
  * pools being DEVICE [num_blocks][Hkv][16][D].  Negative slots are skipped.
- * Slots must be distinct (a repeated slot is a race).  Bit-exact copy. */
+ * Slots must be distinct (a repeated slot is a race).  n < 2^24 per call
+ * (PIC_EINVAL otherwise).  Bit-exact copy. */
 pic_status pic_kv_write(const pic_config* cfg, void* k_pool, void* v_pool, int32_t num_blocks,
                         const void* k_new, const void* v_new, const int32_t* slot_mapping, int32_t n,
                         void* stream);
@@ -166,7 +167,8 @@ pic_status pic_kv_write(const pic_config* cfg, void* k_pool, void* v_pool, int32
  * 16-byte aligned are rejected with PIC_EINVAL.  block_ids is
  * DEVICE [n] and trusted (ids in [0, num_blocks); distinct for a scatter).  One
  * kernel on `stream` copies 16-byte chunks (host buffers are read or written across
- * the host link by the kernel itself); the copies are bit-exact. */
+ * the host link by the kernel itself); the copies are bit-exact.  n < 2^24 blocks
+ * per call (PIC_EINVAL otherwise). */
 pic_status pic_blocks_gather(const pic_config* cfg, const void* k_pool, const void* v_pool, int32_t num_blocks,
                              const int32_t* block_ids, int32_t n, void* dst_k, void* dst_v, void* stream);
 pic_status pic_blocks_scatter(const pic_config* cfg, void* k_pool, void* v_pool, int32_t num_blocks,

@@ -426,6 +426,8 @@ pic_status pic_kv_write(const pic_config* cfg, void* k_pool, void* v_pool, int32
     if (n == 0) return PIC_OK;
     if (!k_pool || !v_pool || !k_new || !v_new || !slot_mapping) return fail(PIC_EINVAL, "NULL buffer");
     if (num_blocks == 0) return fail(PIC_EINVAL, "empty pool");
+    // one workgroup of up to 256 lanes per row: the grid's lane count must stay below 2^32
+    if (n >= (1 << 24)) return fail(PIC_EINVAL, "n must be < 2^24 rows per call");
     return hip_status(pic::launch_kv_write(cfg->dtype, cfg->num_kv_heads, cfg->head_dim, k_pool, v_pool, k_new, v_new,
                                            slot_mapping, n, stream),
                       "kv_write launch");

@@ -108,24 +108,24 @@ __device__ __forceinline__ void rope_cs_n(const float* __restrict__ table, int r
 }
 
 // ---------------------------------------------------------------------------------
-// kv_write: one thread per 16-byte chunk of a new row.
+// kv_write: one workgroup per new row (its slot read once through the scalar unit),
+// one thread per 16-byte chunk of the row's K and V (2^cph_log2 chunks per head).
 // ---------------------------------------------------------------------------------
 __global__ void __launch_bounds__(256) kv_write_kernel(u32x4_t* __restrict__ k_pool, u32x4_t* __restrict__ v_pool,
                                                        const u32x4_t* __restrict__ k_new,
                                                        const u32x4_t* __restrict__ v_new,
-                                                       const int32_t* __restrict__ slots, int64_t n_chunks,
-                                                       int chunks_per_head, int hkv) {
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= n_chunks) return;
-    const int64_t per_row = (int64_t)chunks_per_head * hkv;
-    const int64_t row = i / per_row;
-    const int rem = (int)(i - row * per_row);
-    const int h = rem / chunks_per_head, c = rem - h * chunks_per_head;
-    const int32_t slot = slots[row];
+                                                       const int32_t* __restrict__ slots, int cph_log2, int hkv) {
+    const int64_t row = blockIdx.x;
+    const int32_t slot = __builtin_amdgcn_readfirstlane(slots[row]);
     if (slot < 0) return;
-    const int64_t dst = (((int64_t)(slot >> 4) * hkv + h) * kBlock + (slot & 15)) * chunks_per_head + c;
-    k_pool[dst] = k_new[i];
-    v_pool[dst] = v_new[i];
+    const int per_row = hkv << cph_log2;
+    const int64_t page = ((int64_t)(slot >> 4) * hkv * kBlock + (slot & 15)) << cph_log2;
+    for (int c = threadIdx.x; c < per_row; c += blockDim.x) {
+        const int h = c >> cph_log2, cc = c & ((1 << cph_log2) - 1);
+        const int64_t dst = page + ((int64_t)h * kBlock << cph_log2) + cc;
+        k_pool[dst] = k_new[row * per_row + c];
+        v_pool[dst] = v_new[row * per_row + c];
+    }
 }
 
 // ---------------------------------------------------------------------------------
@@ -1427,15 +1427,16 @@ hipError_t launch_attn_d(int dtype, bool rope, const Plan& plan, const Args& a, 
 
 int launch_kv_write(int dtype, int hkv, int d, void* k_pool, void* v_pool, const void* k_new, const void* v_new,
                     const int32_t* slots, int n, void* stream) {
+    if (n == 0) return hipSuccess;
     const int esize = dtype == 1 ? 4 : 2;
-    const int chunks_per_head = d * esize / 16;
-    const int64_t n_chunks = (int64_t)n * hkv * chunks_per_head;
-    if (n_chunks == 0) return hipSuccess;
-    const int64_t blocks = (n_chunks + 255) / 256;
-    hipLaunchKernelGGL(kv_write_kernel, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream,
+    const int chunks_per_head = d * esize / 16;   // 4, 8, 16 or 32: a power of two
+    int cph_log2 = 0;
+    while ((1 << cph_log2) < chunks_per_head) ++cph_log2;
+    const int per_row = hkv * chunks_per_head;
+    const int threads = per_row >= 256 ? 256 : ((per_row + 63) / 64) * 64;
+    hipLaunchKernelGGL(kv_write_kernel, dim3((unsigned)n), dim3(threads), 0, (hipStream_t)stream,
                        static_cast<u32x4_t*>(k_pool), static_cast<u32x4_t*>(v_pool),
-                       static_cast<const u32x4_t*>(k_new), static_cast<const u32x4_t*>(v_new), slots, n_chunks,
-                       chunks_per_head, hkv);
+                       static_cast<const u32x4_t*>(k_new), static_cast<const u32x4_t*>(v_new), slots, cph_log2, hkv);
     return hipGetLastError();
 }
 

@@ -112,6 +112,7 @@ def test_errors_before_any_hip_call():
     assert lib.pic_blocks_scatter(ctypes.byref(cfg), fake, fake, 4, fake, 1 << 24, fake, fake, None) == B.PIC_EINVAL
     assert lib.pic_blocks_gather(ctypes.byref(P.make_config(4, 3, 64)), fake, fake, 4, fake, 2, fake, fake,
                                  None) == B.PIC_EINVAL
+    assert lib.pic_kv_write(ctypes.byref(cfg), fake, fake, 4, fake, fake, fake, 1 << 24, None) == B.PIC_EINVAL
     # nothing to move: success without a launch
     assert lib.pic_blocks_gather(ctypes.byref(cfg), None, None, 0, None, 0, None, None, None) == B.PIC_OK
     wl = W.config0()
