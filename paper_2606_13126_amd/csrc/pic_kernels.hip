@@ -143,7 +143,28 @@ __global__ void __launch_bounds__(256) blocks_copy_kernel(u32x4_t* __restrict__ 
     u32x4_t* pv = v_pool + b * chunks;
     u32x4_t* bk = k_buf + i * chunks;
     u32x4_t* bv = v_buf + i * chunks;
-    for (int64_t c = threadIdx.x; c < chunks; c += blockDim.x) {
+    // four chunks of K and four of V in flight per thread before any store
+    const int64_t step = blockDim.x;
+    int64_t c = threadIdx.x;
+    for (; c + 3 * step < chunks; c += 4 * step) {
+        u32x4_t kr[4], vr[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            kr[u] = to_pool ? bk[c + u * step] : pk[c + u * step];
+            vr[u] = to_pool ? bv[c + u * step] : pv[c + u * step];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            if (to_pool) {
+                pk[c + u * step] = kr[u];
+                pv[c + u * step] = vr[u];
+            } else {
+                bk[c + u * step] = kr[u];
+                bv[c + u * step] = vr[u];
+            }
+        }
+    }
+    for (; c < chunks; c += step) {
         if (to_pool) {
             pk[c] = bk[c];
             pv[c] = bv[c];
