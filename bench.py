@@ -41,11 +41,14 @@ def flops_of(wl) -> float:
         L = int(wl.seq_lens[r])
         sl = slice(wl.cu_spans[r], wl.cu_spans[r + 1])
         st, fl = wl.span_start[sl], wl.span_flags[sl]
+        sw = None if wl.span_window is None else wl.span_window[sl]
         prev = 0
         for k in range(len(st)):
             b, e = int(st[k]), (int(st[k + 1]) if k + 1 < len(st) else L)
             f = int(fl[k])
             w = b if f & W.SSEP else (0 if f & W.PDEP else prev)
+            if sw is not None and int(sw[k]) >= 0:
+                w = int(sw[k])
             prev = w
             if wl.is_decode:
                 if e == L:

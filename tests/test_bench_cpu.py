@@ -1,0 +1,63 @@
+"""The measurement contract of bench.py, checked on the CPU: algorithmic work and
+bytes against independent counts, the one-GPU refusal, and the traffic figure's
+source check."""
+import json
+import os
+import subprocess
+import sys
+
+import numpy as np
+import pytest
+
+import bench
+import workloads as W
+from oracle import pic_oracle as O
+from tests.cases import windows_prefill_case
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def oracle_flops(wl):
+    p = O.visible_pairs(wl.seq_lens, wl.cu_spans, wl.span_start, wl.span_flags, wl.is_decode, wl.span_window)
+    return 4.0 * wl.head_dim * wl.num_q_heads * p
+
+
+def test_flops_of_the_8b_rag_tail():
+    # 1,343,616 visible (query, key) pairs: 256 tail tokens of a PDEP span after
+    # 5120 cached tokens see 5121..5376 keys each
+    wl = W.config1()
+    pairs = sum(5120 + t + 1 for t in range(256))
+    assert pairs == 1343616
+    assert bench.flops_of(wl) == 4.0 * 128 * 32 * pairs == oracle_flops(wl)
+
+
+@pytest.mark.parametrize("make", [W.config0, lambda: W.config3(num_reqs=4, num_spans=3, span_len=64),
+                                  windows_prefill_case, lambda: W.config2(num_reqs=4, pool_spans=6, per_req=3,
+                                                                          span_len=256, tail=64)])
+def test_flops_of_matches_the_oracle_pair_count(make):
+    wl = make()
+    assert bench.flops_of(wl) == oracle_flops(wl)
+
+
+def test_decode_bytes():
+    wl = W.config3()
+    # 64 requests x 8193 keys x 8 heads x 128 dims x (K + V) x 2 bytes, plus q/o,
+    # positions and block tables
+    kv = 64 * 8193 * 8 * 128 * 2 * 2
+    assert abs(bench.decode_bytes(wl) - kv) / kv < 0.01
+    assert abs(bench.decode_bytes(wl) - 2.151e9) / 2.151e9 < 0.005
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2", "--no-cpu"],
+                       capture_output=True, text=True, timeout=300)
+    assert r.returncode == 2 and "one GPU" in r.stderr
+
+
+def test_traffic_is_reported_only_for_the_measured_sources(monkeypatch):
+    with open(bench.TRAFFIC_FILE) as f:
+        t = json.load(f)
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda: t["source_hash"])
+    assert bench.measured_traffic() == t["bytes_per_call"]
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda: "0" * 16)
+    assert bench.measured_traffic() is None
