@@ -134,6 +134,26 @@ def test_shift_invariance_bf16():
     assert_close(base, ref, wl.dtype, "unshifted vs oracle")
 
 
+@pytest.mark.parametrize("decode", [False, True])
+def test_positions_at_the_int32_limits(decode):
+    # logical positions next to 2^31 - 1 and -2^31: the angle is an exact fixed-point
+    # phase, so attention matches the oracle there (cos/sin computed in the kernel;
+    # the table covers only [0, 1000))
+    if decode:
+        wl = W.small_case("lim_dec", [[Sp(64, S, key="a"), Sp(300, S), Sp(1, Pd, fresh=True)],
+                                      [Sp(64, S, key="a"), Sp(1, Pd, fresh=True)]], Hq=8, Hkv=2, D=128, theta=5e5,
+                          dtype=torch.bfloat16, seed=13, value_scale=0.5, decode=True,
+                          position_offsets=[2**31 - 400, -2**31])
+    else:
+        wl = W.small_case("lim", [[Sp(64, S, key="a"), Sp(300, S | Q, fresh=True), Sp(29, Pd | Q, fresh=True)],
+                                  [Sp(64, S, key="a"), Sp(37, Pd | Q, fresh=True)]], Hq=8, Hkv=2, D=128, theta=5e5,
+                          dtype=torch.bfloat16, seed=13, value_scale=0.5, position_offsets=[2**31 - 400, -2**31])
+    assert int(wl.positions.max()) >= 2**31 - 64 and int(wl.positions.min()) == -2**31
+    say(f"[gpu] int32-limit positions, decode={decode}")
+    got = to_np(gpu_run(wl, table_len=1000).o)
+    assert_close(got, WO.run(wl), wl.dtype, f"int32-limit positions decode={decode}")
+
+
 def test_concurrent_reuse_equals_alone():
     wl = W.config2(num_reqs=4, pool_spans=6, per_req=3, span_len=256, tail=64)
     full = to_np(gpu_run(wl).o)
