@@ -237,7 +237,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-extra", action="store_true")
-    ap.add_argument("--configs", default="2,3,3u,4")
+    ap.add_argument("--workloads", default="concurrent_reuse,decode_64req,decode_64req_unshared,llama3_70b_long",
+                    help="extra workloads (names of workloads.WORKLOADS, or decode_64req_unshared)")
+    ap.add_argument("--no-offload", action="store_true")
     ap.add_argument("--calib", action="store_true", help="also run the 256 MiB calibration copy")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -250,7 +252,7 @@ def main():
     from paper_2606_13126_amd.runner import DeviceBatch
     stream = torch.cuda.current_stream()
 
-    wl = W.config1()
+    wl = W.llama3_8b_rag()
     flops = flops_of(wl)
     db = DeviceBatch(wl, table_positions=table_len(wl))
 
@@ -290,18 +292,18 @@ def main():
     if args.calib:
         calibration_copy()
     if not args.no_extra:
-        extra = {"config1": bench_workload(wl, args.steps, args.warmup, stream)}
-        for c in [x.strip() for x in args.configs.split(",") if x.strip()]:
-            # "3u": the decode workload with every request's spans private (2.15 GB of
-            # unique K/V, the HBM-bound control of the shared-span decode)
-            w = W.config3(shared=False) if c == "3u" else W.make_config(int(c))
-            name = "config3_unshared" if c == "3u" else f"config{c}"
+        extra = {"llama3_8b_rag": bench_workload(wl, args.steps, args.warmup, stream)}
+        for name in [x.strip() for x in args.workloads.split(",") if x.strip()]:
+            # decode_64req_unshared: the decode workload with every request's spans
+            # private (2.15 GB of unique K/V, the HBM-bound control of the shared-span decode)
+            w = W.decode_64req(shared=False) if name == "decode_64req_unshared" else W.make(name)
             extra[name] = bench_workload(w, max(args.steps // 2, 10), max(args.warmup // 2, 3), stream)
             print(f"# {name}: {json.dumps(extra[name])}", file=sys.stderr, flush=True)
             del w
             torch.cuda.empty_cache()
-        extra["offload"] = bench_offload(args.steps, stream)
-        print(f"# offload: {json.dumps(extra['offload'])}", file=sys.stderr, flush=True)
+        if not args.no_offload:
+            extra["offload"] = bench_offload(args.steps, stream)
+            print(f"# offload: {json.dumps(extra['offload'])}", file=sys.stderr, flush=True)
         result["extra"] = extra
     if not args.no_cpu:
         result["cpu_baseline"] = cpu_baseline(wl)

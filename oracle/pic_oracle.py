@@ -22,10 +22,10 @@ around it; Sec. 3.3.1 for how spans are composed in a final request):
   unless given.
 
 Every step is written out in float64 with no blocking or fusion beyond
-chunking the query rows so that score blocks stay small.  Readings of points
-the paper leaves open (RoPE pairing, frequencies, GQA head map, decode
-context) are listed in the design doc; the defaults are NeoX half-split pairing,
-omega_i = theta^(-2i/D), and KV head g = h // (Hq/Hkv).
+chunking the query rows so that score blocks stay small.  Where the paper leaves
+a point open the oracle takes: NeoX half-split pairing (GPT-J on request),
+omega_i = theta^(-2i/D), KV head g = h // (Hq/Hkv), and for decode a query at the
+request's last token, which the call's kv_write has stored.
 """
 from __future__ import annotations
 

@@ -21,7 +21,7 @@ def sample_indices(shape, n, seed):
 
 def main():
     fixtures = {}
-    for name, wl in (("tiny_fp32_prefill", W.config0()), ("tiny_fp32_prefill_tail", W.config0(tail_only=True))):
+    for name, wl in (("tiny_fp32_prefill", W.tiny_fp32()), ("tiny_fp32_prefill_tail", W.tiny_fp32(tail_only=True))):
         o = WO.run(wl)
         idx = sample_indices(o.shape, 48, 99)
         fixtures[name] = {"shape": list(o.shape), "index": idx,

@@ -62,7 +62,7 @@ def batch_of(wl):
 ])
 def test_config_validation(kw, status):
     cfg = P.make_config(**kw)
-    hb = batch_of(W.config0())
+    hb = batch_of(W.tiny_fp32())
     with pytest.raises(P.PicError) as e:
         P.pic_workspace_size(cfg, hb, False)
     assert e.value.status == status
@@ -115,14 +115,14 @@ def test_errors_before_any_hip_call():
     assert lib.pic_kv_write(ctypes.byref(cfg), fake, fake, 4, fake, fake, fake, 1 << 24, None) == B.PIC_EINVAL
     # nothing to move: success without a launch
     assert lib.pic_blocks_gather(ctypes.byref(cfg), None, None, 0, None, 0, None, None, None) == B.PIC_OK
-    wl = W.config0()
+    wl = W.tiny_fp32()
     hb = batch_of(wl)
     dev = B.pic_batch_dev(16, 1, 16)   # max_blocks 1 < 10 blocks of the request
     rc = lib.pic_attn_prefill(ctypes.byref(cfg), ctypes.byref(hb.c), ctypes.byref(dev), None, fake, fake, fake,
                               fake, 16, None, 0, None)
     assert rc == B.PIC_EINVAL and "max_blocks" in lib.pic_last_error().decode()
-    # bf16 config 1 needs split-KV partials: a missing workspace is reported, nothing launched
-    wl1 = W.config1()
+    # the bf16 8B RAG tail needs split-KV partials: a missing workspace is reported, nothing launched
+    wl1 = W.llama3_8b_rag()
     cfg1 = P.make_config(32, 8, 128, rope_theta=5e5)
     dev1 = B.pic_batch_dev(16, 512, 16)
     rc = lib.pic_attn_prefill(ctypes.byref(cfg1), ctypes.byref(batch_of(wl1).c), ctypes.byref(dev1), None, fake,
@@ -176,9 +176,9 @@ def check_exact_cover(wl, dtype, is_decode):
 def test_plan_exact_cover_small(case, dtype):
     S, Pd, Q, Sp = W.SSEP, W.PDEP, W.QUERY, W.Span
     if case == "c0":
-        wl = W.config0()
+        wl = W.tiny_fp32()
     elif case == "c0tail":
-        wl = W.config0(tail_only=True)
+        wl = W.tiny_fp32(tail_only=True)
     elif case == "unaligned":
         wl = W.small_case("u", [[Sp(21, S | Q, fresh=True), Sp(37, S | Q, fresh=True), Sp(11, Pd | Q, fresh=True)]],
                           Hq=8, Hkv=2, D=64)
@@ -191,16 +191,16 @@ def test_plan_exact_cover_small(case, dtype):
     check_exact_cover(wl, dtype, False)
 
 
-def test_plan_exact_cover_config1_and_decode():
-    assert check_exact_cover(W.config1(), B.PIC_BF16, False) == 8 * 256 * 4
-    dec = W.config3(num_reqs=4)
+def test_plan_exact_cover_8b_rag_and_decode():
+    assert check_exact_cover(W.llama3_8b_rag(), B.PIC_BF16, False) == 8 * 256 * 4
+    dec = W.decode_64req(num_reqs=4)
     assert check_exact_cover(dec, B.PIC_BF16, True) == 4 * 8 * 4
 
 
-@pytest.mark.parametrize("cfg_i", [2, 4])
-def test_plan_pair_count_large(cfg_i):
+@pytest.mark.parametrize("name", ["concurrent_reuse", "llama3_70b_long"])
+def test_plan_pair_count_large(name):
     # every item's key range stays inside its rows' windows, and the pairs add up
-    wl = W.make_config(cfg_i)
+    wl = W.make(name)
     G = wl.num_q_heads // wl.num_kv_heads
     cfg = P.make_config(wl.num_q_heads, wl.num_kv_heads, wl.head_dim)
     items = P.pic_plan_debug(cfg, batch_of(wl), False).astype(np.int64)

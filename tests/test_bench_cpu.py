@@ -25,14 +25,14 @@ def oracle_flops(wl):
 def test_flops_of_the_8b_rag_tail():
     # 1,343,616 visible (query, key) pairs: 256 tail tokens of a PDEP span after
     # 5120 cached tokens see 5121..5376 keys each
-    wl = W.config1()
+    wl = W.llama3_8b_rag()
     pairs = sum(5120 + t + 1 for t in range(256))
     assert pairs == 1343616
     assert bench.flops_of(wl) == 4.0 * 128 * 32 * pairs == oracle_flops(wl)
 
 
-@pytest.mark.parametrize("make", [W.config0, lambda: W.config3(num_reqs=4, num_spans=3, span_len=64),
-                                  windows_prefill_case, lambda: W.config2(num_reqs=4, pool_spans=6, per_req=3,
+@pytest.mark.parametrize("make", [W.tiny_fp32, lambda: W.decode_64req(num_reqs=4, num_spans=3, span_len=64),
+                                  windows_prefill_case, lambda: W.concurrent_reuse(num_reqs=4, pool_spans=6, per_req=3,
                                                                           span_len=256, tail=64)])
 def test_flops_of_matches_the_oracle_pair_count(make):
     wl = make()
@@ -40,7 +40,7 @@ def test_flops_of_matches_the_oracle_pair_count(make):
 
 
 def test_decode_bytes():
-    wl = W.config3()
+    wl = W.decode_64req()
     # 64 requests x 8193 keys x 8 heads x 128 dims x (K + V) x 2 bytes, plus q/o,
     # positions and block tables
     kv = 64 * 8193 * 8 * 128 * 2 * 2

@@ -109,7 +109,7 @@ def test_round_trip_new_ids_new_positions(dtype, shift):
 
 
 def test_round_trip_device_buffer_and_decode():
-    wl = W.config3(num_reqs=4, num_spans=3, span_len=64)
+    wl = W.decode_64req(num_reqs=4, num_spans=3, span_len=64)
     db = gpu_run(wl)
     ko, vo = relocate(wl, db, 1234, pinned=False)
     db.attend()
@@ -117,9 +117,9 @@ def test_round_trip_device_buffer_and_decode():
     assert_close(to_np(db.o), WO.run(wl, pools=(ko, vo)), wl.dtype, "offload decode")
 
 
-def test_round_trip_config1_sampled_rows():
+def test_round_trip_8b_rag_sampled_rows():
     # the 8B RAG batch: every cached block leaves and comes back under new ids
-    wl = W.config1()
+    wl = W.llama3_8b_rag()
     db = gpu_run(wl)
     o0 = db.o.clone()
     ko, vo = relocate(wl, db, 0)
@@ -127,7 +127,7 @@ def test_round_trip_config1_sampled_rows():
     torch.cuda.synchronize()
     assert torch.equal(int_view(db.o), int_view(o0))
     rows = np.random.default_rng(2).choice(wl.q.shape[0], 32, replace=False)
-    assert_close(to_np(db.o)[rows], WO.run(wl, rows=rows, pools=(ko, vo)), wl.dtype, "offload config1")
+    assert_close(to_np(db.o)[rows], WO.run(wl, rows=rows, pools=(ko, vo)), wl.dtype, "offload 8B RAG")
 
 
 def test_pageable_host_memory_is_rejected():

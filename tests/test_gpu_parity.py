@@ -34,12 +34,12 @@ def check(wl, style=0, table=True, rows=None, what=None):
 
 @pytest.mark.parametrize("tail_only", [False, True])
 @pytest.mark.parametrize("table", [True, False])
-def test_config0_fp32(tail_only, table):
-    check(W.config0(tail_only=tail_only), table=table)
+def test_tiny_fp32(tail_only, table):
+    check(W.tiny_fp32(tail_only=tail_only), table=table)
 
 
 def test_kv_write_bit_exact():
-    for wl in (W.config0(), W.config1()):
+    for wl in (W.tiny_fp32(), W.llama3_8b_rag()):
         db = gpu_run(wl)
         k_ref, v_ref = wl.k_pool.clone(), wl.v_pool.clone()
         iv = torch.int32 if wl.dtype == torch.float32 else torch.int16
@@ -50,20 +50,20 @@ def test_kv_write_bit_exact():
 
 
 @pytest.mark.parametrize("table", [True, False])
-def test_config1_bf16(table):
-    check(W.config1(), table=table)
+def test_llama3_8b_rag_bf16(table):
+    check(W.llama3_8b_rag(), table=table)
 
 
-def test_config2_bf16():
-    check(W.config2())
+def test_concurrent_reuse_bf16():
+    check(W.concurrent_reuse())
 
 
-def test_config3_decode_bf16():
-    check(W.config3())
+def test_decode_64req_bf16():
+    check(W.decode_64req())
 
 
-def test_config4_sampled_rows():
-    wl = W.config4()
+def test_llama3_70b_long_sampled_rows():
+    wl = W.llama3_70b_long()
     rng = np.random.default_rng(4)
     n = wl.q.shape[0]
     rows = np.unique(np.concatenate([rng.choice(n, 48, replace=False), [0, n - 1, n - 512, n - 513, 511, 512]]))
@@ -155,7 +155,7 @@ def test_positions_at_the_int32_limits(decode):
 
 
 def test_concurrent_reuse_equals_alone():
-    wl = W.config2(num_reqs=4, pool_spans=6, per_req=3, span_len=256, tail=64)
+    wl = W.concurrent_reuse(num_reqs=4, pool_spans=6, per_req=3, span_len=256, tail=64)
     full = to_np(gpu_run(wl).o)
     row = 0
     for r in range(wl.num_reqs):
@@ -177,7 +177,7 @@ def test_concurrent_reuse_equals_alone():
 
 
 def test_decode_equals_prefill_of_last_token():
-    dec = W.config3(num_reqs=3, num_spans=4, span_len=128)
+    dec = W.decode_64req(num_reqs=3, num_spans=4, span_len=128)
     od = to_np(gpu_run(dec).o)
     pre = W.Workload(**{**dec.__dict__})
     pre.is_decode = False

@@ -168,7 +168,7 @@ def test_rope_partial_is_full_rope_of_the_prefix(style):
 def test_variant_attention_is_shift_invariant():
     # any frequencies and a partial width keep scores relative: a shifted request
     # attends the same way
-    wl = W.config0()
+    wl = W.tiny_fp32()
     wl.rotary_dim = 48
     wl.rope_inv_freq = np.linspace(1.0, 1e-3, 24) * 0.9
     o0 = WO.run(wl, style="gptj")
@@ -208,7 +208,7 @@ def test_closed_form_two_dims():
 
 
 def test_first_token_of_ssep_span_returns_its_value():
-    wl = W.config0()
+    wl = W.tiny_fp32()
     o = oracle_of(wl)
     k, v = WO.pools_after_write(wl)
     # q rows are the 160 tokens in order; tokens 0 and 64 each see only themselves
@@ -270,7 +270,7 @@ def test_cached_prefix_then_tail_is_bottom_right_causal():
 
 @pytest.mark.parametrize("shift", [1, -37, 1000, 65536, 100003])
 def test_shift_invariance(shift):
-    wl = W.config0()
+    wl = W.tiny_fp32()
     o0 = oracle_of(wl)
     wl.positions = wl.positions + np.int32(shift)
     o1 = oracle_of(wl)
@@ -278,7 +278,7 @@ def test_shift_invariance(shift):
 
 
 def test_block_permutation_invariance():
-    wl = W.config0()
+    wl = W.tiny_fp32()
     o0 = oracle_of(wl)
     perm = RNG.permutation(wl.num_blocks)           # new id of old block b is perm[b]
     inv = np.argsort(perm)
@@ -388,7 +388,7 @@ def test_offload_and_reload_under_new_ids_keeps_outputs():
     # Sec. 3.2.3: blocks leave the pool (here to a bf16-width byte buffer standing in for
     # host memory), come back under different ids into a pool whose other blocks hold
     # garbage, and the block table is the only thing updated: outputs are unchanged
-    wl = W.config0()
+    wl = W.tiny_fp32()
     k, v = WO.pools_after_write(wl)
     o0 = oracle_of(wl)
     used = np.unique(wl.block_tables[wl.block_tables >= 0])
@@ -482,11 +482,11 @@ def test_planted_gqa_map_is_caught(monkeypatch):
 
 def test_config_work_counts():
     # visible-pair counts of the five workloads (4*D*Hq*P flops for prefill)
-    assert O.visible_pairs(*[getattr(W.config0(), a) for a in ("seq_lens", "cu_spans", "span_start",
+    assert O.visible_pairs(*[getattr(W.tiny_fp32(), a) for a in ("seq_lens", "cu_spans", "span_start",
                                                                  "span_flags")]) == 8784
-    wl = W.config0(tail_only=True)
+    wl = W.tiny_fp32(tail_only=True)
     assert O.visible_pairs(wl.seq_lens, wl.cu_spans, wl.span_start, wl.span_flags) == 4624
-    wl = W.config1()
+    wl = W.llama3_8b_rag()
     assert O.visible_pairs(wl.seq_lens, wl.cu_spans, wl.span_start, wl.span_flags) == 1343616
 
 
@@ -496,7 +496,7 @@ def test_stored_oracle_fixture():
     path = os.path.join(os.path.dirname(__file__), "golden", "oracle_tiny_fp32.json")
     with open(path) as f:
         fx = json.load(f)
-    for name, wl in (("tiny_fp32_prefill", W.config0()), ("tiny_fp32_prefill_tail", W.config0(tail_only=True))):
+    for name, wl in (("tiny_fp32_prefill", W.tiny_fp32()), ("tiny_fp32_prefill_tail", W.tiny_fp32(tail_only=True))):
         o = oracle_of(wl)
         ref = fx[name]
         assert list(o.shape) == ref["shape"]

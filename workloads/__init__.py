@@ -240,7 +240,7 @@ def build(name: str, requests: Sequence[Sequence[Span]], *, num_q_heads: int, nu
 # The five benchmark-shaped workloads
 # ----------------------------------------------------------------------------------------
 
-def config0(seed: int = 1000, tail_only: bool = False) -> Workload:
+def tiny_fp32(seed: int = 1000, tail_only: bool = False) -> Workload:
     """Tiny fp32 prefill: two SSEP spans of 64 tokens and a 32-token PDEP tail,
     4 query heads over 1 KV head, head_dim 64, theta 1e4, 16 pool blocks of which
     10 are used in shuffled order.  All 160 tokens are queries (fresh), or only the
@@ -255,7 +255,7 @@ def config0(seed: int = 1000, tail_only: bool = False) -> Workload:
                  dtype=torch.float32, seed=seed, value_scale=1.0, num_blocks=16)
 
 
-def config1(seed: int = 1001) -> Workload:
+def llama3_8b_rag(seed: int = 1001) -> Workload:
     """Llama-3-8B-shaped RAG prefill: 10 cached SSEP spans of 512 tokens and a fresh
     256-token PDEP query tail; 32/8 heads, head_dim 128, theta 5e5, bf16."""
     spans = [Span(512, SSEP, key=("doc", i)) for i in range(10)] + [Span(256, PDEP | QUERY, fresh=True)]
@@ -263,7 +263,7 @@ def config1(seed: int = 1001) -> Workload:
                  rope_theta=5e5, dtype=torch.bfloat16, seed=seed, value_scale=0.5, num_blocks=512)
 
 
-def config2(seed: int = 1002, num_reqs: int = 16, pool_spans: int = 32, per_req: int = 8,
+def concurrent_reuse(seed: int = 1002, num_reqs: int = 16, pool_spans: int = 32, per_req: int = 8,
             span_len: int = 512, tail: int = 128) -> Workload:
     """Concurrent reuse: each of 16 requests draws 8 of 32 shared cached spans
     (without replacement, random order) plus a private 128-token PDEP query tail."""
@@ -278,7 +278,7 @@ def config2(seed: int = 1002, num_reqs: int = 16, pool_spans: int = 32, per_req:
                  rope_theta=5e5, dtype=torch.bfloat16, seed=seed, value_scale=0.5, num_blocks=nb)
 
 
-def config3(seed: int = 1003, num_reqs: int = 64, num_spans: int = 16, span_len: int = 512,
+def decode_64req(seed: int = 1003, num_reqs: int = 64, num_spans: int = 16, span_len: int = 512,
             shared: bool = True) -> Workload:
     """Decode: 64 requests, each an 8192-token context of 16 shared 512-token spans in a
     per-request random order, plus the new token (written through the slot mapping)
@@ -301,7 +301,7 @@ def config3(seed: int = 1003, num_reqs: int = 64, num_spans: int = 16, span_len:
                  num_blocks=nb, decode=True, poison=shared)
 
 
-def config4(seed: int = 1004, num_spans: int = 64, span_len: int = 512, tail: int = 512) -> Workload:
+def llama3_70b_long(seed: int = 1004, num_spans: int = 64, span_len: int = 512, tail: int = 512) -> Workload:
     """Llama-3-70B-shaped long prefill: 64 SSEP spans of 512 tokens, a seeded half of
     them fresh (queried and written in the call), the other half cached, and a fresh
     512-token PDEP query tail; 64/8 heads, head_dim 128, theta 5e5, bf16."""
@@ -320,11 +320,13 @@ def config4(seed: int = 1004, num_spans: int = 64, span_len: int = 512, tail: in
                  rope_theta=5e5, dtype=torch.bfloat16, seed=seed, value_scale=0.5, num_blocks=nb)
 
 
-CONFIGS = {0: config0, 1: config1, 2: config2, 3: config3, 4: config4}
+WORKLOADS = {"tiny_fp32": tiny_fp32, "llama3_8b_rag": llama3_8b_rag, "concurrent_reuse": concurrent_reuse,
+             "decode_64req": decode_64req, "llama3_70b_long": llama3_70b_long}
 
 
-def make_config(i: int, **kw) -> Workload:
-    return CONFIGS[i](**kw)
+def make(name: str, **kw) -> Workload:
+    """The named workload (a key of WORKLOADS)."""
+    return WORKLOADS[name](**kw)
 
 
 def small_case(name: str, requests: Sequence[Sequence[Span]], *, Hq=4, Hkv=2, D=64, theta=1e4,
