@@ -358,9 +358,17 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
     const int li = bid - g.item_base;
     if (li >= n_clusters * g.n_rt) return;
     int cluster, rt;
-    if ((n_clusters & 7) == 0) {
-        // blocks bid, bid+8, ... run on one XCD: give them the row tiles of one
-        // (KV head, split) so that they share K/V in that XCD's L2
+    if ((a.hkv & 7) == 0) {
+        // blocks bid, bid+8, ... run on one XCD: give them every (split, row tile) of
+        // one KV head, so that the row tiles share K/V and the splits share Q in that
+        // XCD's L2
+        const int per_kvh = g.n_split * g.n_rt;
+        const int x = li & 7, k = li >> 3;
+        const int kv = x + 8 * (k / per_kvh), r = k % per_kvh;
+        cluster = kv * g.n_split + r / g.n_rt;
+        rt = r % g.n_rt;
+    } else if ((n_clusters & 7) == 0) {
+        // the same for the row tiles of one (KV head, split)
         const int x = li & 7, k = li >> 3;
         cluster = x + 8 * (k / g.n_rt);
         rt = k % g.n_rt;
