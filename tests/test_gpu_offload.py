@@ -145,3 +145,24 @@ def test_pageable_host_memory_is_rejected():
     db.attend()
     torch.cuda.synchronize()
     assert torch.isfinite(db.o.float()).all()
+
+
+def test_misaligned_buffer_is_rejected():
+    # the copies move 16-byte chunks: a buffer starting 2 bytes into an allocation is
+    # refused on the host, before any launch
+    from paper_2606_13126_amd import _binding as B
+    wl = shared_span_case(torch.bfloat16)
+    db = gpu_run(wl)
+    ids = torch.zeros(1, dtype=torch.int32, device="cuda")
+    flat = torch.empty(db.k_pool[0].numel() + 8, dtype=db.k_pool.dtype, device="cuda")
+    dst = flat[1:1 + db.k_pool[0].numel()].view((1,) + tuple(db.k_pool.shape[1:]))
+    say("[gpu] offload: misaligned destination (host-side rejection)")
+    with pytest.raises(B.PicError) as e:
+        B.pic_blocks_gather(db.cfg, db.k_pool, db.v_pool, ids, dst, dst)
+    assert e.value.status == B.PIC_EINVAL and "aligned" in str(e.value)
+    # the same buffer aligned works, and empty requests are no-ops
+    B.pic_blocks_gather(db.cfg, db.k_pool, db.v_pool, ids[:0], dst, dst)
+    ok = flat[8:8 + db.k_pool[0].numel()].view((1,) + tuple(db.k_pool.shape[1:]))
+    B.pic_blocks_gather(db.cfg, db.k_pool, db.v_pool, ids, ok, ok)
+    torch.cuda.synchronize()
+    assert torch.equal(ok.cpu().view(torch.int16), db.v_pool[0:1].cpu().view(torch.int16))
