@@ -285,6 +285,16 @@ def test_decode_prerotated_equals_fused():
     assert_close(to_np(fused.o), WO.run(wl), wl.dtype, "fused decode vs oracle")
 
 
+@pytest.mark.parametrize("style,table", [(0, True), (1, False)])
+def test_decode_fp32(style, table):
+    # fp32 decode runs the fp32 kernel (one wave per query and head): max-abs 1e-4
+    wl = decode_case(8, 2, 128, seed=17)
+    wl.dtype = torch.float32
+    for name in ("q", "k_pool", "v_pool", "k_new", "v_new"):
+        setattr(wl, name, getattr(wl, name).float())
+    check(wl, style=style, table=table, what=f"fp32 decode style={style} table={table}")
+
+
 @pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
 def test_generalised_windows_prefill(dtype):
     check(windows_prefill_case(dtype), what=f"generalised windows {dtype}")
