@@ -43,6 +43,12 @@ __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b) {
                                            false);
 }
 
+// (a.lo, b.lo) and (a.hi, b.hi) of two bf16 pairs: the rotate-half pairing brings
+// element i of one 8-dim run together with element i of the run half a head
+// further; one byte permute each (bytes 0-3 of the selector pick from a, 4-7 from b)
+__device__ __forceinline__ uint32_t pair_lo(uint32_t a, uint32_t b) { return __builtin_amdgcn_perm(b, a, 0x05040100u); }
+__device__ __forceinline__ uint32_t pair_hi(uint32_t a, uint32_t b) { return __builtin_amdgcn_perm(b, a, 0x07060302u); }
+
 // c + a.lo + a.hi for a pair of bf16 values (a dot product with (1, 1), one
 // accumulate-in-place instruction)
 __device__ __forceinline__ float sum2_bf16(uint32_t a, float c) {
@@ -578,8 +584,8 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
 #pragma unroll
             for (int m = 0; m < 4; ++m) {
                 const uint32_t A = r.k[0][m], B = r.k[1][m];
-                const uint32_t p0 = (A & 0xffffu) | (B << 16);        // (x_2m, y_2m)
-                const uint32_t p1 = (A >> 16) | (B & 0xffff0000u);    // (x_2m+1, y_2m+1)
+                const uint32_t p0 = pair_lo(A, B);   // (x_2m, y_2m)
+                const uint32_t p1 = pair_hi(A, B);   // (x_2m+1, y_2m+1)
                 const float x0 = dot2_bf16(p0, e[2 * m].x), y0 = dot2_bf16(p0, e[2 * m].y);
                 const float x1 = dot2_bf16(p1, e[2 * m + 1].x), y1 = dot2_bf16(p1, e[2 * m + 1].y);
                 r.k[0][m] = pack_bf16(x0, x1);
@@ -595,10 +601,9 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
                     r.k[h2][m] = pack_bf16(dot2_bf16(xy, ee.x), dot2_bf16(xy, ee.y));
                 }
         }
-        // keys outside the window (partial tiles only) are stored as zeros
-        if (__builtin_amdgcn_ballot_w64(!r.ok) != 0) {
-            if (!r.ok) r.k[0] = r.k[1] = u32x4_t{0, 0, 0, 0};
-        }
+        // a key outside the window (partial tiles only) was loaded as zeros and its
+        // entries e are finite (the table's, or the last tile's, or zero), so it is
+        // stored as zeros; its score is masked in any case
         const int sw = swz<D>(kr);
         uint16_t* krow = &ks[buf][kr * D];
         const int ca = STYLE == kNeox ? sc : 2 * sc;
@@ -611,6 +616,8 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
     // ---- prologue: the queries' loads and the first tile's loads are all in flight
     // before the first wait
     TileRegs regs[SU];
+#pragma unroll
+    for (int u = 0; u < SU; ++u) regs[u] = TileRegs{};   // entries start finite
     q_issue();
     dma_meta(0);
     dma_meta(1);
@@ -1169,7 +1176,7 @@ __global__ void __launch_bounds__(dec_heads(D) * 64, 1) decode_bf16(const Plan p
 #pragma unroll
                     for (int m = 0; m < 4; ++m) {
                         const uint32_t A = kf[kd][m], B = kf[kd + KD / 2][m];
-                        const uint32_t p0 = (A & 0xffffu) | (B << 16), p1 = (A >> 16) | (B & 0xffff0000u);
+                        const uint32_t p0 = pair_lo(A, B), p1 = pair_hi(A, B);
                         const u32x4_t e = te[kd * 4 + m];   // pairs 2m, 2m+1 of this 8-dim run
                         kf[kd][m] = pack_bf16(dot2_bf16(p0, e[0]), dot2_bf16(p1, e[2]));
                         kf[kd + KD / 2][m] = pack_bf16(dot2_bf16(p0, e[1]), dot2_bf16(p1, e[3]));
