@@ -24,6 +24,9 @@
  *    null stream).  Kernel execution errors surface at the caller's next sync.
  *  - Tensors are dense and row-major in the shapes given.  Q, O, the K/V pools
  *    and new K/V rows share cfg->dtype.
+ *  - Tensors (Q, O, pools, new rows, rope tables, the workspace) start on 16-byte
+ *    boundaries and int32 arrays on 4-byte boundaries; other addresses are
+ *    rejected with PIC_EINVAL before anything is launched.
  */
 #ifndef PIC_ATTN_H
 #define PIC_ATTN_H

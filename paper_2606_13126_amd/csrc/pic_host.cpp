@@ -29,6 +29,10 @@ pic_status fail(pic_status st, const std::string& msg) {
     return st;
 }
 
+// The kernels move 16-byte chunks of every tensor (some of them straight into LDS)
+// and 4-byte words of the int32 arrays: addresses that do not allow it are refused.
+static bool misaligned(const void* p, uintptr_t to) { return p != nullptr && reinterpret_cast<uintptr_t>(p) % to != 0; }
+
 pic_status check_config(const pic_config* c) {
     if (c == nullptr) return fail(PIC_EINVAL, "cfg is NULL");
     if (c->num_q_heads <= 0 || c->num_kv_heads <= 0) return fail(PIC_EINVAL, "head counts must be positive");
@@ -327,6 +331,11 @@ pic_status run_attention(const pic_config* c, const pic_batch_host* b, const pic
             return fail(PIC_EINVAL, "max_blocks too small for seq_lens[" + std::to_string(r) + "]");
     if (!k_pool || !v_pool) return fail(PIC_EINVAL, "pools must not be NULL");
     if (rope != nullptr && rope->data != nullptr && rope->len < 0) return fail(PIC_EINVAL, "rope table len < 0");
+    if (misaligned(q, 16) || misaligned(o, 16) || misaligned(k_pool, 16) || misaligned(v_pool, 16) ||
+        misaligned(ws, 16) || (rope != nullptr && misaligned(rope->data, 16)))
+        return fail(PIC_EINVAL, "q, o, the pools, the workspace and the rope table must be 16-byte aligned");
+    if (misaligned(dv->block_tables, 4) || misaligned(dv->positions, 4))
+        return fail(PIC_EINVAL, "block tables and positions must be 4-byte aligned");
 
     HostPlan hp;
     if ((st = make_plan(c, b, decode, hp))) return st;
@@ -394,6 +403,7 @@ pic_status pic_rope_table_build(const pic_config* cfg, int32_t num_positions, vo
     if (st) return st;
     if (num_positions < 0) return fail(PIC_EINVAL, "num_positions < 0");
     if (num_positions > 0 && table == nullptr) return fail(PIC_EINVAL, "table is NULL");
+    if (misaligned(table, 16)) return fail(PIC_EINVAL, "table must be 16-byte aligned");
     pic::RopeSteps steps;
     phase_steps(cfg, steps.s);
     return hip_status(pic::launch_rope_table(cfg->dtype, cfg->head_dim, steps, num_positions,
@@ -408,6 +418,8 @@ pic_status pic_rope_rotate(const pic_config* cfg, const pic_rope_table* rope, vo
     if (n < 0 || num_heads <= 0) return fail(PIC_EINVAL, "bad n or num_heads");
     if (n == 0) return PIC_OK;
     if (x == nullptr || positions == nullptr) return fail(PIC_EINVAL, "x and positions must not be NULL");
+    if (misaligned(x, 16) || misaligned(positions, 4) || (rope != nullptr && misaligned(rope->data, 16)))
+        return fail(PIC_EINVAL, "x and the rope table must be 16-byte aligned, positions 4-byte aligned");
     const bool table = rope != nullptr && rope->data != nullptr && rope->len > 0;
     pic::RopeSteps steps;
     phase_steps(cfg, steps.s);
@@ -426,6 +438,9 @@ pic_status pic_kv_write(const pic_config* cfg, void* k_pool, void* v_pool, int32
     if (n == 0) return PIC_OK;
     if (!k_pool || !v_pool || !k_new || !v_new || !slot_mapping) return fail(PIC_EINVAL, "NULL buffer");
     if (num_blocks == 0) return fail(PIC_EINVAL, "empty pool");
+    if (misaligned(k_pool, 16) || misaligned(v_pool, 16) || misaligned(k_new, 16) || misaligned(v_new, 16) ||
+        misaligned(slot_mapping, 4))
+        return fail(PIC_EINVAL, "pools and new rows must be 16-byte aligned, slot_mapping 4-byte aligned");
     // one workgroup of up to 256 lanes per row: the grid's lane count must stay below 2^32
     if (n >= (1 << 24)) return fail(PIC_EINVAL, "n must be < 2^24 rows per call");
     return hip_status(pic::launch_kv_write(cfg->dtype, cfg->num_kv_heads, cfg->head_dim, k_pool, v_pool, k_new, v_new,

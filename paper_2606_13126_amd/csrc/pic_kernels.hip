@@ -289,6 +289,14 @@ struct TileRegs {
 // wait until this wave's global loads (including loads into LDS) have landed
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
+// s_waitcnt on vector memory only: wait until at most N loads of this wave are
+// outstanding (they complete in issue order)
+template <int N>
+__device__ __forceinline__ void wait_vmem_n() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
 typedef __attribute__((address_space(3))) void lds_void_t;
 
 // Global -> LDS copies written as inline assembly (global_load_lds_dword[x4], LDS
@@ -415,20 +423,19 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
         const uint16_t* qp = static_cast<const uint16_t*>(a.q) +
                              ((size_t)(g.q_row0 + toff) * a.hq + (size_t)kvh * G + hl) * D;
 #pragma unroll
-        for (int kd = 0; kd < KD; ++kd)
-            qraw[kd] = row_valid ? *reinterpret_cast<const u32x4_t*>(qp + model_chunk(a.chunk_map, 2 * kd + hi) * 8)
-                                 : u32x4_t{0, 0, 0, 0};
+        for (int kd = 0; kd < KD; ++kd)   // KD loads on every lane (a row past the tile reads the group's first)
+            qraw[kd] = *reinterpret_cast<const u32x4_t*>(qp + model_chunk(a.chunk_map, 2 * kd + hi) * 8);
         if (ROPE && row_valid) qpos = a.positions[g.pos_off + g.tok0 + toff];
     };
     auto q_finish = [&]() {   // rotate, scale by softmax_scale*log2(e), round to bf16
-        const u32x4_t* raw = qraw;
         float xf[KD][8];
 #pragma unroll
         for (int kd = 0; kd < KD; ++kd)
 #pragma unroll
             for (int m = 0; m < 4; ++m) {
-                xf[kd][2 * m] = bf_lo(raw[kd][m]);
-                xf[kd][2 * m + 1] = bf_hi(raw[kd][m]);
+                const uint32_t w = row_valid ? qraw[kd][m] : 0u;
+                xf[kd][2 * m] = bf_lo(w);
+                xf[kd][2 * m + 1] = bf_hi(w);
             }
         if (ROPE) {
             const int32_t pos = qpos;
@@ -618,11 +625,13 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
     TileRegs regs[SU];
 #pragma unroll
     for (int u = 0; u < SU; ++u) regs[u] = TileRegs{};   // entries start finite
-    q_issue();
     dma_meta(0);
     dma_meta(1);
-    wait_vmem();
-    __syncthreads();   // metadata of tiles 0 and 1 landed; phase steps staged
+    q_issue();
+    // the metadata copies (issued before the KD query loads, which may still be in
+    // flight) have landed, and the phase steps are staged
+    wait_vmem_n<KD>();
+    barrier_keep_vmem();
     issue_direct(0, 0);
     load_tile(0, regs);
     q_finish();
@@ -791,12 +800,12 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
 // ---------------------------------------------------------------------------------
 // merge: O = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s over the non-empty splits
 // of one (row tile, KV head), as a streaming log-sum-exp merge.  One block per
-// kMergeRows rows, one float4 of a row per thread; the loads of 8 splits are issued
+// kMergeRows rows, 8 dims (16 bytes of bf16) of a row per thread; the loads of 8 splits are issued
 // together before they are combined.
 // ---------------------------------------------------------------------------------
 template <int D>
-__global__ void __launch_bounds__(kMergeRows * D / 4) merge_kernel(const Plan plan, const Args a) {
-    constexpr int TPR = D / 4;                      // threads per row
+__global__ void __launch_bounds__(kMergeRows * D / 8) merge_kernel(const Plan plan, const Args a) {
+    constexpr int TPR = D / 8;                      // threads per row, 8 dims (16 bytes) each
     constexpr int CHUNKS = kTileRows / kMergeRows;  // blocks per (row tile, KV head)
     constexpr int U = 8;                            // splits loaded per batch
     const int gi = plan_search<&Group::merge_base>(plan, blockIdx.x);
@@ -816,23 +825,23 @@ __global__ void __launch_bounds__(kMergeRows * D / 4) merge_kernel(const Plan pl
     for (int s = 0; s < g.n_split; ++s)
         if (g.win + s * g.split_keys < t_last + 1) n_live = s + 1;
     const int r = chunk * kMergeRows + (int)threadIdx.x / TPR;
-    const int q4 = (int)threadIdx.x % TPR;
+    const int q8 = (int)threadIdx.x % TPR;
     if (row_lo + r >= row_hi) return;
     const size_t slot0 = (size_t)part_base + (size_t)kvh * g.n_split * g.n_rt + rt;
     float M = kNegBig, den = 0.f;
-    float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
+    float num[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     const uint16_t* part = reinterpret_cast<const uint16_t*>(a.part_o);
     for (int s0 = 0; s0 < n_live; s0 += U) {
         float2 ml[U];
-        u32x2_t v[U];
+        u32x4_t v[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             ml[u] = make_float2(kNegBig, 0.f);
-            v[u] = u32x2_t{0, 0};
+            v[u] = u32x4_t{0, 0, 0, 0};
             if (s0 + u < n_live) {
                 const size_t slot = slot0 + (size_t)(s0 + u) * g.n_rt;
                 ml[u] = *reinterpret_cast<const float2*>(a.part_ml + (slot * kTileRows + r) * 2);
-                v[u] = *reinterpret_cast<const u32x2_t*>(part + (slot * kTileRows + r) * D + q4 * 4);
+                v[u] = *reinterpret_cast<const u32x4_t*>(part + (slot * kTileRows + r) * D + q8 * 8);
             }
         }
         // each split's output is normalised: weight it by its sum times 2^(m_s - M)
@@ -842,10 +851,11 @@ __global__ void __launch_bounds__(kMergeRows * D / 4) merge_kernel(const Plan pl
             const float m_new = fmaxf(M, ml[u].x);
             const float c_old = __builtin_amdgcn_exp2f(M - m_new);
             const float w = __builtin_amdgcn_exp2f(ml[u].x - m_new) * ml[u].y;
-            num.x = num.x * c_old + w * bf_lo(v[u][0]);
-            num.y = num.y * c_old + w * bf_hi(v[u][0]);
-            num.z = num.z * c_old + w * bf_lo(v[u][1]);
-            num.w = num.w * c_old + w * bf_hi(v[u][1]);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                num[2 * e] = num[2 * e] * c_old + w * bf_lo(v[u][e]);
+                num[2 * e + 1] = num[2 * e + 1] * c_old + w * bf_hi(v[u][e]);
+            }
             den = den * c_old + w;
             M = m_new;
         }
@@ -853,10 +863,11 @@ __global__ void __launch_bounds__(kMergeRows * D / 4) merge_kernel(const Plan pl
     const float inv = 1.f / den;
     const int row = row_lo + r;
     const int toff = row / G, hl = row - toff * G;
-    uint32_t* op = reinterpret_cast<uint32_t*>(static_cast<uint16_t*>(a.o) +
-                                               ((size_t)(g.q_row0 + toff) * a.hq + (size_t)kvh * G + hl) * D + q4 * 4);
-    op[0] = pack_bf16(num.x * inv, num.y * inv);
-    op[1] = pack_bf16(num.z * inv, num.w * inv);
+    u32x4_t out;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) out[e] = pack_bf16(num[2 * e] * inv, num[2 * e + 1] * inv);
+    *reinterpret_cast<u32x4_t*>(static_cast<uint16_t*>(a.o) + ((size_t)(g.q_row0 + toff) * a.hq + (size_t)kvh * G + hl) * D +
+                                q8 * 8) = out;
 }
 
 // ---------------------------------------------------------------------------------
@@ -871,14 +882,6 @@ __device__ __forceinline__ float max_xor16(float x) {
 __device__ __forceinline__ float sum_xor16(float x) {
     const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-
-// s_waitcnt on vector memory only: wait until at most N loads of this wave are
-// outstanding (they complete in issue order)
-template <int N>
-__device__ __forceinline__ void wait_vmem_n() {
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
 // A wave-uniform element read through the scalar unit (the value lands in an
@@ -1426,7 +1429,7 @@ hipError_t launch_attn_t(int dtype, const Plan& plan, const Args& a, hipStream_t
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (plan.n_merge > 0) {
-        hipLaunchKernelGGL((merge_kernel<D>), dim3(plan.n_merge), dim3(kMergeRows * D / 4), 0, st, plan, a);
+        hipLaunchKernelGGL((merge_kernel<D>), dim3(plan.n_merge), dim3(kMergeRows * D / 8), 0, st, plan, a);
         e = hipGetLastError();
     }
     return e;

@@ -95,6 +95,37 @@ def test_batch_validation(mut):
     assert e.value.status == B.PIC_EINVAL
 
 
+def test_misaligned_addresses_are_rejected_before_any_hip_call():
+    # the kernels move 16-byte chunks (some straight into LDS) and 4-byte words of the
+    # int32 arrays: other addresses are refused on the host, nothing is launched
+    cfg = P.make_config(4, 1, 64)
+    lib = B.lib()
+    ok, off8, off2 = ctypes.c_void_p(256), ctypes.c_void_p(264), ctypes.c_void_p(258)
+
+    def refused(rc):
+        return rc == B.PIC_EINVAL and "aligned" in lib.pic_last_error().decode()
+
+    assert refused(lib.pic_kv_write(ctypes.byref(cfg), off8, ok, 4, ok, ok, ok, 3, None))
+    assert refused(lib.pic_kv_write(ctypes.byref(cfg), ok, ok, 4, ok, off8, ok, 3, None))
+    assert refused(lib.pic_kv_write(ctypes.byref(cfg), ok, ok, 4, ok, ok, off2, 3, None))
+    assert refused(lib.pic_rope_rotate(ctypes.byref(cfg), None, off8, 5, 2, ok, None))
+    assert refused(lib.pic_rope_rotate(ctypes.byref(cfg), None, ok, 5, 2, off2, None))
+    assert refused(lib.pic_rope_table_build(ctypes.byref(cfg), 8, off8, None))
+    hb = batch_of(W.tiny_fp32())
+    for q, o, kp, vp in ((off8, ok, ok, ok), (ok, off8, ok, ok), (ok, ok, off8, ok), (ok, ok, ok, off8)):
+        dev = B.pic_batch_dev(256, 16, 256)
+        assert refused(lib.pic_attn_prefill(ctypes.byref(cfg), ctypes.byref(hb.c), ctypes.byref(dev), None, q, o, kp,
+                                            vp, 16, None, 0, None))
+    for bt, pos in ((258, 256), (256, 258)):
+        dev = B.pic_batch_dev(bt, 16, pos)
+        assert refused(lib.pic_attn_decode(ctypes.byref(cfg), ctypes.byref(hb.c), ctypes.byref(dev), None, ok, ok, ok,
+                                           ok, 16, None, 0, None))
+    table = B.pic_rope_table(264, 160)
+    dev = B.pic_batch_dev(256, 16, 256)
+    assert refused(lib.pic_attn_prefill(ctypes.byref(cfg), ctypes.byref(hb.c), ctypes.byref(dev), ctypes.byref(table),
+                                        ok, ok, ok, ok, 16, None, 0, None))
+
+
 def test_errors_before_any_hip_call():
     # invalid calls return before touching the device, so they are safe without a GPU
     cfg = P.make_config(4, 1, 64)
