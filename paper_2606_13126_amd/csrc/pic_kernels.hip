@@ -122,15 +122,28 @@ __global__ void __launch_bounds__(256) kv_write_kernel(u32x4_t* __restrict__ k_p
                                                        const u32x4_t* __restrict__ v_new,
                                                        const int32_t* __restrict__ slots, int cph_log2, int hkv) {
     const int64_t row = blockIdx.x;
+    const int per_row = hkv << cph_log2;
+    // the thread's first chunk is read together with the slot (one round trip)
+    const int c0 = threadIdx.x;
+    u32x4_t k0 = u32x4_t{0, 0, 0, 0}, v0 = u32x4_t{0, 0, 0, 0};
+    if (c0 < per_row) {
+        k0 = k_new[row * per_row + c0];
+        v0 = v_new[row * per_row + c0];
+    }
     const int32_t slot = __builtin_amdgcn_readfirstlane(slots[row]);
     if (slot < 0) return;
-    const int per_row = hkv << cph_log2;
     const int64_t page = ((int64_t)(slot >> 4) * hkv * kBlock + (slot & 15)) << cph_log2;
-    for (int c = threadIdx.x; c < per_row; c += blockDim.x) {
+    auto dst_of = [&](int c) {
         const int h = c >> cph_log2, cc = c & ((1 << cph_log2) - 1);
-        const int64_t dst = page + ((int64_t)h * kBlock << cph_log2) + cc;
-        k_pool[dst] = k_new[row * per_row + c];
-        v_pool[dst] = v_new[row * per_row + c];
+        return page + ((int64_t)h * kBlock << cph_log2) + cc;
+    };
+    if (c0 < per_row) {
+        k_pool[dst_of(c0)] = k0;
+        v_pool[dst_of(c0)] = v0;
+    }
+    for (int c = c0 + (int)blockDim.x; c < per_row; c += blockDim.x) {
+        k_pool[dst_of(c)] = k_new[row * per_row + c];
+        v_pool[dst_of(c)] = v_new[row * per_row + c];
     }
 }
 
