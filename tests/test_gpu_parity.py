@@ -79,6 +79,22 @@ def test_unaligned_spans_gqa(style, dtype):
     check(wl, style=style)
 
 
+@pytest.mark.parametrize("Hq,Hkv,D,style", [
+    (12, 4, 128, 0),    # G = 3: 256-row tiles end inside a token's heads
+    (14, 2, 64, 1),     # G = 7
+    (24, 2, 128, 1),    # G = 12
+    (48, 3, 64, 0),     # G = 16, three KV heads (no XCD grouping of KV heads)
+])
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_prefill_query_groups_straddling_row_tiles(Hq, Hkv, D, style, dtype):
+    # query rows are (token, head) pairs; with G not dividing the 256-row tile the
+    # heads of one token are split between two workgroups
+    reqs = [[Sp(48, S, key="a"), Sp(100, S | Q, fresh=True), Sp(61, Pd | Q, fresh=True)],
+            [Sp(48, S, key="a"), Sp(23, Pd | Q, fresh=True)]]
+    wl = W.small_case("groups", reqs, Hq=Hq, Hkv=Hkv, D=D, theta=1e4, dtype=dtype, seed=40 + Hq, value_scale=0.5)
+    check(wl, style=style)
+
+
 @pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
 def test_mha_d64_multi_request(dtype):
     reqs = [[Sp(64, S, key="a"), Sp(48, S, key="b"), Sp(70, Pd | Q, fresh=True)],
