@@ -231,7 +231,7 @@ def cpu_baseline(wl, budget_s=12.0):
         WO.run(wl)
         runs += 1
         el = time.perf_counter() - t0
-        if el >= budget_s or runs >= 20:
+        if el >= budget_s or runs >= 500:
             break
     per = el / runs
     return {"value": flops_of(wl) / per / 1e12, "unit": "TFLOP/s", "cores": int(blas or cores),
