@@ -775,39 +775,45 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
         if (t + 1 < n_tiles) step(std::integral_constant<int, 1>{}, t + 1);
     }
 
-    // ---- epilogue: normalise and store, or store the split's partial state
+    // ---- epilogue: normalise (a split by its own sum, its running maximum and sum
+    // stored beside it), round to bf16 and store.  The rows pass through this wave's
+    // own 32 rows of the now idle K/V tile buffers (chunks XOR-swizzled by row), so
+    // that each global store writes whole 16-byte chunks of 64 / CH complete rows.
     const float lt = sum_xor32(l_run);
-    if (!row_valid) return;
-    if (g.n_split == 1) {
-        const float inv = 1.f / lt;
-        uint16_t* op = static_cast<uint16_t*>(a.o) + ((size_t)(g.q_row0 + toff) * a.hq + (size_t)kvh * G + hl) * D;
+    if (!wave_live) return;
+    const bool is_split = g.n_split > 1;
+    const float inv = lt > 0.f ? 1.f / lt : 0.f;
+    uint16_t* stage = (wave < kWaves / 2 ? &ks[0][0] : &vs[0][0]) + (wave % (kWaves / 2)) * 32 * D;
+    static_assert(2 * BN >= 32 * (kWaves / 2), "epilogue staging rows");
 #pragma unroll
-        for (int db = 0; db < DB; ++db)
+    for (int db = 0; db < DB; ++db)
 #pragma unroll
-            for (int q4 = 0; q4 < 4; ++q4) {
-                const int d = db * 32 + 8 * q4 + 4 * hi;
-                const u32x2_t w = {pack_bf16(acc[db][4 * q4] * inv, acc[db][4 * q4 + 1] * inv),
-                                   pack_bf16(acc[db][4 * q4 + 2] * inv, acc[db][4 * q4 + 3] * inv)};
-                *reinterpret_cast<u32x2_t*>(op + d) = w;
-            }
-    } else {
-        // the split's output normalised by its own sum, in bf16 (half the partial
-        // traffic of fp32), with the split's running maximum and sum beside it
-        const size_t slot = (size_t)part_base + (size_t)cluster * g.n_rt + rt;
-        uint16_t* po = reinterpret_cast<uint16_t*>(a.part_o) + (slot * kTileRows + (row - row_lo)) * D;
-        const float inv = lt > 0.f ? 1.f / lt : 0.f;
+        for (int q4 = 0; q4 < 4; ++q4) {
+            const int c = db * 4 + q4;   // dims 8c .. 8c+7 of the row; this lane holds half of them
+            const u32x2_t w = {pack_bf16(acc[db][4 * q4] * inv, acc[db][4 * q4 + 1] * inv),
+                               pack_bf16(acc[db][4 * q4 + 2] * inv, acc[db][4 * q4 + 3] * inv)};
+            *reinterpret_cast<u32x2_t*>(stage + l32 * D + ((c ^ (l32 & (CH - 1))) << 3) + 4 * hi) = w;
+        }
+    __builtin_amdgcn_wave_barrier();
+    const size_t slot = (size_t)part_base + (size_t)cluster * g.n_rt + rt;
+    constexpr int RPI = 64 / CH;   // rows per store instruction
 #pragma unroll
-        for (int db = 0; db < DB; ++db)
-#pragma unroll
-            for (int q4 = 0; q4 < 4; ++q4) {
-                const int d = db * 32 + 8 * q4 + 4 * hi;
-                const u32x2_t w = {pack_bf16(acc[db][4 * q4] * inv, acc[db][4 * q4 + 1] * inv),
-                                   pack_bf16(acc[db][4 * q4 + 2] * inv, acc[db][4 * q4 + 3] * inv)};
-                *reinterpret_cast<u32x2_t*>(po + d) = w;
-            }
-        if (hi == 0)
-            *reinterpret_cast<float2*>(a.part_ml + (slot * kTileRows + (row - row_lo)) * 2) = make_float2(m_run, lt);
+    for (int i = 0; i < 32 / RPI; ++i) {
+        const int r = i * RPI + lane / CH, c = lane % CH;
+        const u32x4_t v = *reinterpret_cast<const u32x4_t*>(stage + r * D + ((c ^ (r & (CH - 1))) << 3));
+        const int rr = wave_row0 + r;
+        if (rr >= row_hi) continue;
+        uint16_t* dst;
+        if (is_split) {
+            dst = reinterpret_cast<uint16_t*>(a.part_o) + (slot * kTileRows + (rr - row_lo)) * D;
+        } else {
+            const int to = rr / G, h = rr - to * G;
+            dst = static_cast<uint16_t*>(a.o) + ((size_t)(g.q_row0 + to) * a.hq + (size_t)kvh * G + h) * D;
+        }
+        *reinterpret_cast<u32x4_t*>(dst + c * 8) = v;
     }
+    if (is_split && hi == 0 && row_valid)
+        *reinterpret_cast<float2*>(a.part_ml + (slot * kTileRows + (row - row_lo)) * 2) = make_float2(m_run, lt);
 }
 
 // ---------------------------------------------------------------------------------
