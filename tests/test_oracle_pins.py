@@ -550,3 +550,45 @@ def test_planted_ignored_window_override_is_caught(monkeypatch):
     monkeypatch.setattr(O, "span_windows", lambda a, b, c, span_window=None: orig(a, b, c, None))
     with pytest.raises(AssertionError):
         test_nback_window_equals_subrequest()
+
+
+# ---- row / request subsets ------------------------------------------------------------
+# The GPU parity tests of the largest workloads ask the oracle for a subset of the query
+# rows (prefill) or requests (decode).  The subset branch selects, reorders and scatters
+# rows, so it is pinned directly against the brute force, in the order asked for.
+
+def test_prefill_row_subset_equals_bruteforce_rows():
+    reqs = TINY["shared_two_reqs"] + [[Sp(9, S | Q, fresh=True), Sp(7, Q, fresh=True), Sp(4, P | Q, fresh=True)]]
+    wl = W.small_case("subset", reqs, Hq=4, Hkv=2, D=8, theta=10.0, seed=21)
+    b = brute_of(wl)
+    n = b.shape[0]
+    for rows in (np.array([n - 1, 0, 5, 3]),                      # unsorted, both ends
+                 np.array([7, 6, 5, 4]),                           # descending inside request 1
+                 RNG.permutation(n)[: n // 2],                     # random half, any order
+                 np.arange(n)[::-1]):                              # every row, reversed
+        got = oracle_of(wl, rows=rows)
+        assert got.shape == (len(rows),) + b.shape[1:]
+        assert np.max(np.abs(got - b[rows])) <= 1e-12, rows
+
+
+def test_decode_request_subset_equals_bruteforce_requests():
+    reqs = [[Sp(16, S, key="a"), Sp(16, S, key="b"), Sp(1, P, fresh=True)],
+            [Sp(16, S, key="b"), Sp(7, S), Sp(1, 0, fresh=True)],
+            [Sp(5, P), Sp(1, S, fresh=True)],
+            [Sp(16, S, key="a"), Sp(3, 0, fresh=True)]]
+    wl = W.small_case("dec_subset", reqs, Hq=6, Hkv=3, D=8, theta=100.0, seed=6, decode=True)
+    b = brute_of(wl)
+    for sel in ([3, 0], [2], [1, 3, 0, 2], [0, 1, 2, 3]):
+        got = oracle_of(wl, rows=sel)
+        assert got.shape == (len(sel),) + b.shape[1:]
+        assert np.max(np.abs(got - b[sel])) <= 1e-12, sel
+
+
+def test_planted_subset_misorder_is_caught():
+    # a subset branch that returned rows in sorted order instead of the order asked
+    # for would fail the pins above: check that such a mistake is visible
+    wl = W.small_case("subset_mut", TINY["ssep_pdep"], Hq=4, Hkv=2, D=8, theta=10.0, seed=22)
+    b = brute_of(wl)
+    rows = np.array([30, 2, 17])
+    wrong = oracle_of(wl, rows=np.sort(rows))
+    assert np.max(np.abs(wrong - b[rows])) > 1e-3
