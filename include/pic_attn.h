@@ -179,8 +179,10 @@ pic_status pic_blocks_scatter(const pic_config* cfg, void* k_pool, void* v_pool,
                               void* stream);
 
 /* Workspace bytes that pic_attn_prefill (is_decode = 0) or pic_attn_decode
- * (is_decode = 1) needs for this configuration and batch (split-KV partial
- * results).  May be 0. */
+ * (is_decode = 1) needs for this configuration and batch: split-KV partial results
+ * and, for batches of more than 64 groups (query spans; requests for decode), the
+ * work-group table that the call writes there before its attention launch.  May be
+ * 0.  Returned through *bytes (the status reports argument errors). */
 pic_status pic_workspace_size(const pic_config* cfg, const pic_batch_host* batch, int32_t is_decode,
                               size_t* bytes);
 
@@ -215,6 +217,14 @@ pic_status pic_attn_decode(const pic_config* cfg, const pic_batch_host* batch, c
  * and the full count to *n_items.  No HIP call is made. */
 pic_status pic_plan_debug(const pic_config* cfg, const pic_batch_host* batch, int32_t is_decode,
                           int32_t* items, int32_t capacity, int32_t* n_items);
+
+/* Test hook: the launch shape of the prefill/decode call (HOST int32 shape[5]):
+ * {blocks of the attention launch, blocks of the split-merge launch (0: none),
+ *  groups (query spans, or requests for decode), plan-upload launches that write the
+ *  group table into the workspace (0 when the groups travel as kernel arguments),
+ *  split partial slots}.  Every call is one attention launch and at most one merge
+ *  launch, whatever the batch size.  No HIP call is made. */
+pic_status pic_plan_shape(const pic_config* cfg, const pic_batch_host* batch, int32_t is_decode, int32_t* shape);
 
 #ifdef __cplusplus
 }

@@ -73,6 +73,7 @@ _sig = {
     "pic_attn_decode": (c_int32, [_P(pic_config), _P(pic_batch_host), _P(pic_batch_dev), _P(pic_rope_table),
                                   c_void_p, c_void_p, c_void_p, c_void_p, c_int32, c_void_p, c_size_t, c_void_p]),
     "pic_plan_debug": (c_int32, [_P(pic_config), _P(pic_batch_host), c_int32, _P(c_int32), c_int32, _P(c_int32)]),
+    "pic_plan_shape": (c_int32, [_P(pic_config), _P(pic_batch_host), c_int32, _P(c_int32)]),
     # span cache (include/pic_cache.h): host only
     "pic_sha256": (c_int32, [c_void_p, c_size_t, c_void_p]),
     "pic_block_hashes": (c_int32, [c_void_p, c_int32, c_int32, c_int32, c_void_p, c_void_p]),
@@ -226,6 +227,13 @@ def pic_plan_debug(cfg: pic_config, batch: HostBatch, is_decode: bool) -> np.nda
     _check(_lib.pic_plan_debug(ctypes.byref(cfg), ctypes.byref(batch.c), int(is_decode),
                                out.ctypes.data_as(POINTER(c_int32)), n.value, ctypes.byref(n)))
     return out[: n.value]
+
+
+def pic_plan_shape(cfg: pic_config, batch: HostBatch, is_decode: bool) -> dict:
+    out = (c_int32 * 5)()
+    _check(_lib.pic_plan_shape(ctypes.byref(cfg), ctypes.byref(batch.c), int(is_decode), out))
+    return {"attention_blocks": out[0], "merge_blocks": out[1], "groups": out[2], "upload_launches": out[3],
+            "partial_slots": out[4]}
 
 
 # ------------------------------------------------------------------------------------

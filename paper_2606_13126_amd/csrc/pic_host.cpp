@@ -4,8 +4,12 @@
 // The planner turns the host span descriptor into launch groups: one group per
 // PIC_QUERY span (prefill) or per request (decode), each with its window start
 // (Sec. 3.1.1: SSEP -> span start, PDEP -> 0, unflagged -> previous span's
-// window), its row tiles and its key splits.  Groups travel to the kernels by
-// value as a kernel argument, so a call enqueues no host-to-device copy.
+// window), its row tiles and its key splits.  A call is one attention launch (and
+// one merge launch when keys are split) whatever the batch size.  Up to
+// kMaxGroups groups travel to the kernels by value as a kernel argument; larger
+// batches get their group table written into the caller's workspace by small
+// plan-upload launches whose arguments carry the groups.  No call enqueues a
+// host-to-device copy.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -21,6 +25,7 @@ namespace {
 
 // both structures travel as kernel arguments
 static_assert(sizeof(pic::Plan) + sizeof(pic::Args) <= 4096, "kernel arguments must stay within 4 KB");
+static_assert(sizeof(pic::PlanUpload) <= 4096, "kernel arguments must stay within 4 KB");
 
 thread_local std::string g_error;
 
@@ -109,7 +114,9 @@ pic_status check_batch(const pic_batch_host* b) {
 
 struct HostPlan {
     std::vector<pic::Group> groups;
-    int64_t n_parts = 0;
+    int64_t n_items = 0;       // blocks of the attention launch
+    int64_t n_parts = 0;       // split partial slots
+    int64_t n_merge = 0;       // blocks of the merge launch
     bool dec_kernel = false;   // decode through the one-query kernel (bf16, G <= 16)
 };
 
@@ -225,46 +232,65 @@ int64_t items_of(const pic_config* c, const HostPlan& hp, const pic::Group& g) {
     return (int64_t)g.n_rt * c->num_kv_heads * g.n_split;
 }
 
-// Cut the group list into launches of at most kMaxGroups groups and assign bases.
-void make_launches(const pic_config* c, HostPlan& hp, std::vector<pic::Plan>& launches) {
-    launches.clear();
-    int64_t part = 0;
-    size_t i = 0;
-    while (i < hp.groups.size()) {
-        pic::Plan p;
-        std::memset(&p, 0, sizeof(p));
-        p.part0 = (int32_t)part;
-        int64_t item = 0, merge = 0;
-        while (i < hp.groups.size() && p.n_groups < pic::kMaxGroups) {
-            pic::Group g = hp.groups[i];
-            const int64_t n = items_of(c, hp, g);
-            const int64_t n_pad = hp.dec_kernel ? n : round_up(n, 8);
-            if (item + n_pad > INT32_MAX / 2 && p.n_groups > 0) break;
-            g.item_base = (int32_t)item;
-            g.part_base = (int32_t)part;
-            g.merge_base = (int32_t)merge;
-            item += n_pad;
-            if (hp.dec_kernel) {
-                if (g.n_split > 1) {
-                    part += n;
-                    merge += (c->num_q_heads + pic::kMergeRows - 1) / pic::kMergeRows;
-                }
-            } else if (c->dtype != PIC_F32 && g.n_split > 1) {
-                part += (int64_t)g.n_rt * c->num_kv_heads * g.n_split;
-                merge += (int64_t)g.n_rt * c->num_kv_heads * (pic::kTileRows / pic::kMergeRows);
+// Assign every group its item, partial-slot and merge-block bases (one attention
+// launch and one merge launch for the whole call) and count the blocks.
+pic_status assign_bases(const pic_config* c, HostPlan& hp) {
+    int64_t item = 0, part = 0, merge = 0;
+    for (auto& g : hp.groups) {
+        const int64_t n = items_of(c, hp, g);
+        const int64_t n_pad = hp.dec_kernel ? n : round_up(n, 8);
+        g.item_base = (int32_t)item;
+        g.part_base = (int32_t)part;
+        g.merge_base = (int32_t)merge;
+        item += n_pad;
+        if (hp.dec_kernel) {
+            if (g.n_split > 1) {
+                part += n;
+                merge += (c->num_q_heads + pic::kMergeRows - 1) / pic::kMergeRows;
             }
-            p.g[p.n_groups++] = g;
-            ++i;
+        } else if (c->dtype != PIC_F32 && g.n_split > 1) {
+            part += (int64_t)g.n_rt * c->num_kv_heads * g.n_split;
+            merge += (int64_t)g.n_rt * c->num_kv_heads * (pic::kTileRows / pic::kMergeRows);
         }
-        p.n_items = (int32_t)item;
-        p.n_merge = (int32_t)merge;
-        launches.push_back(p);
+        // a launch's lanes (blocks x threads) must stay below 2^31
+        if (item > (1 << 22) || merge > (1 << 23) || part > (1 << 24))
+            return fail(PIC_EINVAL, "batch too large for one call (split it into several calls)");
     }
+    hp.n_items = item;
     hp.n_parts = part;
+    hp.n_merge = merge;
+    return PIC_OK;
 }
 
-size_t workspace_bytes(const pic_config* c, int64_t n_parts) {
-    return (size_t)n_parts * pic::kTileRows * ((size_t)c->head_dim + 2) * sizeof(float);
+constexpr size_t kWsAlign = 256;
+size_t align_up(size_t x) { return (x + kWsAlign - 1) / kWsAlign * kWsAlign; }
+
+// Workspace layout: split partial outputs [n_parts][kTileRows][D] (sized for fp32),
+// their (max, sum) pairs [n_parts][kTileRows][2], and -- for batches of more than
+// kMaxGroups groups -- the group table with the block -> group maps.
+struct WsLayout {
+    size_t ml = 0, table = 0, item_map = 0, merge_map = 0, total = 0;
+};
+
+WsLayout ws_layout(const pic_config* c, const HostPlan& hp) {
+    WsLayout w;
+    const size_t parts = (size_t)hp.n_parts * pic::kTileRows;
+    w.ml = parts * c->head_dim * sizeof(float);
+    w.total = w.ml + parts * 2 * sizeof(float);
+    if (hp.groups.size() > (size_t)pic::kMaxGroups) {
+        w.table = align_up(w.total);
+        w.item_map = align_up(w.table + hp.groups.size() * sizeof(pic::Group));
+        w.merge_map = align_up(w.item_map + (size_t)hp.n_items * sizeof(int32_t));
+        w.total = w.merge_map + (size_t)hp.n_merge * sizeof(int32_t);
+    }
+    return w;
+}
+
+// The plan of a call: groups with their split policy, then their bases.
+pic_status build_plan(const pic_config* c, const pic_batch_host* b, bool decode, HostPlan& hp) {
+    pic_status st = make_plan(c, b, decode, hp);
+    if (st) return st;
+    return assign_bases(c, hp);
 }
 
 // Phase step of RoPE pair i: omega_i / 2pi revolutions per position as a 64-bit
@@ -338,16 +364,14 @@ pic_status run_attention(const pic_config* c, const pic_batch_host* b, const pic
         return fail(PIC_EINVAL, "block tables and positions must be 4-byte aligned");
 
     HostPlan hp;
-    if ((st = make_plan(c, b, decode, hp))) return st;
+    if ((st = build_plan(c, b, decode, hp))) return st;
     int64_t rows = 0;
     for (auto& g : hp.groups) rows += g.n_tok;
     if (rows == 0) return PIC_OK;
     if (!q || !o) return fail(PIC_EINVAL, "q and o must not be NULL");
-    std::vector<pic::Plan> launches;
-    make_launches(c, hp, launches);
-    const size_t need = workspace_bytes(c, hp.n_parts);
-    if (need > 0 && (ws == nullptr || ws_bytes < need))
-        return fail(PIC_EWORKSPACE, "workspace needs " + std::to_string(need) + " bytes");
+    const WsLayout wl = ws_layout(c, hp);
+    if (wl.total > 0 && (ws == nullptr || ws_bytes < wl.total))
+        return fail(PIC_EWORKSPACE, "workspace needs " + std::to_string(wl.total) + " bytes");
 
     pic::Args a{};
     phase_steps(c, a.fstep);
@@ -361,21 +385,53 @@ pic_status run_attention(const pic_config* c, const pic_batch_host* b, const pic
     const bool table = rope != nullptr && rope->data != nullptr && rope->len > 0;
     a.rope_table = table ? static_cast<const float*>(rope->data) : nullptr;
     a.rope_len = table ? rope->len : 0;
-    a.part_o = static_cast<float*>(ws);
-    a.part_ml = hp.n_parts ? static_cast<float*>(ws) + (size_t)hp.n_parts * pic::kTileRows * c->head_dim : nullptr;
+    char* wsb = static_cast<char*>(ws);
+    a.part_o = hp.n_parts ? reinterpret_cast<float*>(wsb) : nullptr;
+    a.part_ml = hp.n_parts ? reinterpret_cast<float*>(wsb + wl.ml) : nullptr;
     const double scale = c->softmax_scale > 0.f ? (double)c->softmax_scale : 1.0 / std::sqrt((double)c->head_dim);
     a.scale_log2 = (float)(scale * 1.4426950408889634);
     a.max_blocks = dv->max_blocks;
     a.hq = c->num_q_heads;
     a.hkv = c->num_kv_heads;
     a.group = c->num_q_heads / c->num_kv_heads;
-    for (const auto& p : launches) {
-        const bool rope_on = c->k_prerotated == 0;
-        const int e = hp.dec_kernel ? pic::launch_decode(c->rope_style, c->head_dim, rope_on, p, a, stream)
-                                    : pic::launch_attention(c->dtype, c->rope_style, c->head_dim, rope_on, p, a, stream);
-        if ((st = hip_status(e, "attention launch"))) return st;
+
+    pic::Plan p;
+    std::memset(&p, 0, sizeof(p));
+    p.n_groups = (int32_t)hp.groups.size();
+    p.n_items = (int32_t)hp.n_items;
+    p.n_merge = (int32_t)hp.n_merge;
+    if (hp.groups.size() <= (size_t)pic::kMaxGroups) {
+        std::copy(hp.groups.begin(), hp.groups.end(), p.g);
+    } else {
+        // the group table and block maps go to the workspace, written on the stream
+        // ahead of the attention launch by plan-upload launches of up to
+        // kUploadGroups groups each (their arguments carry the groups)
+        pic::Group* tab = reinterpret_cast<pic::Group*>(wsb + wl.table);
+        int32_t* imap = reinterpret_cast<int32_t*>(wsb + wl.item_map);
+        int32_t* mmap = reinterpret_cast<int32_t*>(wsb + wl.merge_map);
+        p.table = tab;
+        p.item_map = imap;
+        p.merge_map = mmap;
+        const size_t n = hp.groups.size();
+        for (size_t first = 0; first < n; first += pic::kUploadGroups) {
+            pic::PlanUpload u;
+            std::memset(&u, 0, sizeof(u));
+            u.table = tab;
+            u.item_map = imap;
+            u.merge_map = mmap;
+            u.first = (int32_t)first;
+            u.n = (int32_t)std::min<size_t>(pic::kUploadGroups, n - first);
+            std::copy(hp.groups.begin() + first, hp.groups.begin() + first + u.n, u.g);
+            const bool last = first + u.n == n;
+            u.item_end = last ? (int32_t)hp.n_items : hp.groups[first + u.n].item_base;
+            u.merge_end = last ? (int32_t)hp.n_merge : hp.groups[first + u.n].merge_base;
+            if ((st = hip_status(pic::launch_plan_upload(u, stream), "plan upload launch"))) return st;
+        }
     }
-    return PIC_OK;
+    const bool rope_on = c->k_prerotated == 0;
+    const int e = hp.dec_kernel ? pic::launch_decode(c->rope_style, c->head_dim, rope_on, p, a, stream)
+                                : pic::launch_attention(c->dtype, c->rope_style, c->head_dim, rope_on, p, a, stream);
+    return hip_status(e, "attention launch");
 }
 
 }  // namespace
@@ -512,10 +568,8 @@ pic_status pic_workspace_size(const pic_config* cfg, const pic_batch_host* batch
     if ((st = check_batch(batch))) return st;
     if (bytes == nullptr) return fail(PIC_EINVAL, "bytes is NULL");
     HostPlan hp;
-    if ((st = make_plan(cfg, batch, is_decode != 0, hp))) return st;
-    std::vector<pic::Plan> launches;
-    make_launches(cfg, hp, launches);
-    *bytes = workspace_bytes(cfg, hp.n_parts);
+    if ((st = build_plan(cfg, batch, is_decode != 0, hp))) return st;
+    *bytes = ws_layout(cfg, hp).total;
     return PIC_OK;
 }
 
@@ -541,9 +595,7 @@ pic_status pic_plan_debug(const pic_config* cfg, const pic_batch_host* batch, in
     if (n_items == nullptr || capacity < 0 || (capacity > 0 && items == nullptr))
         return fail(PIC_EINVAL, "bad output arguments");
     HostPlan hp;
-    if ((st = make_plan(cfg, batch, is_decode != 0, hp))) return st;
-    std::vector<pic::Plan> launches;
-    make_launches(cfg, hp, launches);
+    if ((st = build_plan(cfg, batch, is_decode != 0, hp))) return st;
     const int G = cfg->num_q_heads / cfg->num_kv_heads;
     int64_t n = 0;
     auto emit = [&](int32_t r, int32_t h, int32_t rl, int32_t rh, int32_t kl, int32_t kh, int32_t t0, int32_t slot) {
@@ -553,9 +605,9 @@ pic_status pic_plan_debug(const pic_config* cfg, const pic_batch_host* batch, in
         }
         ++n;
     };
-    for (const auto& p : launches) {
-        for (int gi = 0; gi < p.n_groups; ++gi) {
-            const pic::Group& g = p.g[gi];
+    {
+        for (size_t gi = 0; gi < hp.groups.size(); ++gi) {
+            const pic::Group& g = hp.groups[gi];
             if (hp.dec_kernel) {
                 const int64_t n_hg = dec_head_groups(cfg);
                 for (int s = 0; s < g.n_split; ++s) {
@@ -594,6 +646,22 @@ pic_status pic_plan_debug(const pic_config* cfg, const pic_batch_host* batch, in
         }
     }
     *n_items = (int32_t)std::min<int64_t>(n, INT32_MAX);
+    return PIC_OK;
+}
+
+pic_status pic_plan_shape(const pic_config* cfg, const pic_batch_host* batch, int32_t is_decode, int32_t* shape) {
+    pic_status st = check_config(cfg);
+    if (st) return st;
+    if ((st = check_batch(batch))) return st;
+    if (shape == nullptr) return fail(PIC_EINVAL, "shape is NULL");
+    HostPlan hp;
+    if ((st = build_plan(cfg, batch, is_decode != 0, hp))) return st;
+    const int64_t n = (int64_t)hp.groups.size();
+    shape[0] = (int32_t)hp.n_items;
+    shape[1] = (int32_t)hp.n_merge;
+    shape[2] = (int32_t)n;
+    shape[3] = n > pic::kMaxGroups ? (int32_t)((n + pic::kUploadGroups - 1) / pic::kUploadGroups) : 0;
+    shape[4] = (int32_t)hp.n_parts;
     return PIC_OK;
 }
 

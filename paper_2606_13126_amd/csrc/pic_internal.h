@@ -16,7 +16,8 @@ constexpr int kBlock = 16;        // tokens per KV block
 #endif
 constexpr int kTileRows = PIC_TILE_ROWS;  // query rows (token x head-in-group) per prefill workgroup
 constexpr int kTileKeys = PIC_TILE_KEYS;  // keys per K/V tile of the prefill kernel
-constexpr int kMaxGroups = 72;    // groups passed by value in one launch (kernel arguments < 4 KB)
+constexpr int kMaxGroups = 64;    // groups passed by value as a kernel argument (arguments < 4 KB)
+constexpr int kUploadGroups = 80; // groups carried by one plan-upload launch
 constexpr int kTargetCUs = 256;   // MI355X compute units the split policy fills
 constexpr int kMergeRows = 8;     // rows per block of the split merge
 constexpr int kDecTileKeys = 16;  // keys per decode tile (one cache block)
@@ -32,8 +33,8 @@ constexpr int dec_heads(int head_dim) { return head_dim == 128 ? PIC_DEC_HEADS_D
 // group) for the decode kernel -- enumerated from item_base.  Partial results of
 // split groups take consecutive slots from part_base, and their merge blocks
 // consecutive block indices of the merge launch from merge_base.  item_base and
-// merge_base are non-decreasing over a launch's groups, so a block finds its group
-// by binary search.
+// merge_base are non-decreasing over the groups, so with the groups in the kernel
+// arguments a block finds its group by binary search.
 struct Group {
     int32_t req;         // request index (row of the block table)
     int32_t tok0;        // sequence index of the span's first query token
@@ -49,12 +50,34 @@ struct Group {
     int32_t merge_base;  // first block of the merge launch (split groups)
 };
 
+// The work of one call: one attention launch of n_items blocks and one merge launch
+// of n_merge blocks, whatever the number of groups.  Up to kMaxGroups groups travel
+// in g[] (binary-searched by the blocks); a larger batch has its groups in the
+// caller's workspace (`table`), written there by plan-upload launches on the same
+// stream, with the group index of every attention block in item_map and of every
+// merge block in merge_map.
 struct Plan {
     int32_t n_groups;
     int32_t n_items;     // blocks of the attention launch
     int32_t n_merge;     // blocks of the merge launch
-    int32_t part0;       // first partial slot of this launch's split groups
+    int32_t pad_;
+    const Group* table;       // device [n_groups], or null when g[] holds the groups
+    const int32_t* item_map;  // device [n_items]: group of each attention block
+    const int32_t* merge_map; // device [n_merge]: group of each merge block
     Group g[kMaxGroups];
+};
+
+// Arguments of one plan-upload launch: groups [first, first + n) of the call, and
+// where the block ranges of the chunk's last group end.
+struct PlanUpload {
+    Group* table;
+    int32_t* item_map;
+    int32_t* merge_map;
+    int32_t first;
+    int32_t n;
+    int32_t item_end;
+    int32_t merge_end;
+    Group g[kUploadGroups];
 };
 
 // last group whose `field` is <= b (the fields are non-decreasing over groups)
@@ -114,5 +137,6 @@ int launch_rope_rotate(int dtype, int style, int d, int rot_half, const RopeStep
                        int n, int heads, const int32_t* positions, void* stream);
 int launch_attention(int dtype, int style, int d, bool rope, const Plan& plan, const Args& args, void* stream);
 int launch_decode(int style, int d, bool rope, const Plan& plan, const Args& args, void* stream);
+int launch_plan_upload(const PlanUpload& up, void* stream);
 
 }  // namespace pic

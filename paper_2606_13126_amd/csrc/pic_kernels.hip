@@ -243,12 +243,42 @@ __global__ void __launch_bounds__(256) rope_rotate_kernel(T* __restrict__ x, int
     row[ib] = (T)(b * c + a * s);
 }
 
-// Partial slots and merge blocks of a split group.
-// Group of an attention block and its first partial slot.
-__device__ __forceinline__ int find_group(const Plan& plan, int bid, int& part_base) {
-    const int gi = plan_search<&Group::item_base>(plan, bid);
-    part_base = plan.g[gi].part_base;
-    return gi;
+// A wave-uniform element read through the scalar unit (the value lands in an
+// SGPR and waits on the scalar counter, not on the vector-memory queue).
+typedef __attribute__((address_space(4))) const int32_t const_i32_t;
+__device__ __forceinline__ int32_t scalar_load(const int32_t* p, int i) { return ((const_i32_t*)p)[i]; }
+
+// Group of attention block `bid` (MERGE: of merge block `bid`): binary search over
+// the groups in the kernel arguments, or two scalar loads from the table the
+// plan-upload launches wrote for a large batch.
+template <bool MERGE>
+__device__ __forceinline__ Group group_of(const Plan& plan, int bid) {
+    if (plan.table != nullptr) {
+        const int gi = scalar_load(MERGE ? plan.merge_map : plan.item_map, bid);
+        const int32_t* src = reinterpret_cast<const int32_t*>(plan.table + gi);
+        Group g;
+        int32_t* dst = reinterpret_cast<int32_t*>(&g);
+#pragma unroll
+        for (int k = 0; k < (int)(sizeof(Group) / 4); ++k) dst[k] = scalar_load(src, k);
+        return g;
+    }
+    return plan.g[MERGE ? plan_search<&Group::merge_base>(plan, bid) : plan_search<&Group::item_base>(plan, bid)];
+}
+
+// ---------------------------------------------------------------------------------
+// plan_upload: block i writes group first + i of a large batch into the table and
+// its index into the block -> group maps of the attention and merge launches.
+// ---------------------------------------------------------------------------------
+__global__ void __launch_bounds__(256) plan_upload_kernel(const PlanUpload u) {
+    const int i = blockIdx.x;
+    const Group& g = u.g[i];
+    const int item_end = i + 1 < u.n ? u.g[i + 1].item_base : u.item_end;
+    const int merge_end = i + 1 < u.n ? u.g[i + 1].merge_base : u.merge_end;
+    const int gi = u.first + i;
+    if (threadIdx.x < sizeof(Group) / 4)
+        reinterpret_cast<int32_t*>(u.table + gi)[threadIdx.x] = reinterpret_cast<const int32_t*>(&g)[threadIdx.x];
+    for (int b = g.item_base + (int)threadIdx.x; b < item_end; b += blockDim.x) u.item_map[b] = gi;
+    for (int b = g.merge_base + (int)threadIdx.x; b < merge_end; b += blockDim.x) u.merge_map[b] = gi;
 }
 
 constexpr int kWaves = kTileRows / 32;   // wave w owns rows [32w, 32w+32); 2 waves per SIMD
@@ -378,8 +408,8 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
     const int l32 = lane & 31, hi = lane >> 5;
 
     const int bid = blockIdx.x;
-    int part_base;
-    const Group g = plan.g[find_group(plan, bid, part_base)];
+    const Group g = group_of<false>(plan, bid);
+    const int part_base = g.part_base;
     const int G = a.group;
     const int n_clusters = a.hkv * g.n_split;
     const int li = bid - g.item_base;
@@ -827,8 +857,7 @@ __global__ void __launch_bounds__(kMergeRows * D / 8) merge_kernel(const Plan pl
     constexpr int TPR = D / 8;                      // threads per row, 8 dims (16 bytes) each
     constexpr int CHUNKS = kTileRows / kMergeRows;  // blocks per (row tile, KV head)
     constexpr int U = 8;                            // splits loaded per batch
-    const int gi = plan_search<&Group::merge_base>(plan, blockIdx.x);
-    const Group g = plan.g[gi];
+    const Group g = group_of<true>(plan, blockIdx.x);
     const int part_base = g.part_base, merge_base = g.merge_base;
     if (g.n_split <= 1) return;
     int li = blockIdx.x - merge_base;
@@ -902,11 +931,6 @@ __device__ __forceinline__ float sum_xor16(float x) {
     const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
-
-// A wave-uniform element read through the scalar unit (the value lands in an
-// SGPR and waits on the scalar counter, not on the vector-memory queue).
-typedef __attribute__((address_space(4))) const int32_t const_i32_t;
-__device__ __forceinline__ int32_t scalar_load(const int32_t* p, int i) { return ((const_i32_t*)p)[i]; }
 
 template <int D>
 constexpr int dec_stages() {
@@ -993,8 +1017,8 @@ __global__ void __launch_bounds__(dec_heads(D) * 64, 1) decode_bf16(const Plan p
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int c16 = lane & 15, q4 = lane >> 4;   // MFMA column (query / key row) and row group
     const int n_hg = (a.hkv + HW - 1) / HW;
-    int part_base;
-    const Group g = plan.g[find_group(plan, blockIdx.x, part_base)];
+    const Group g = group_of<false>(plan, blockIdx.x);
+    const int part_base = g.part_base;
     const int li = blockIdx.x - g.item_base;
     if (li >= g.n_split * n_hg) return;
     const int split = li / n_hg, hg = li - (li / n_hg) * n_hg;
@@ -1305,7 +1329,7 @@ __global__ void __launch_bounds__(kMergeRows * D / 4) decode_merge(const Plan pl
     constexpr int HW = dec_heads(D);
     constexpr int U = 8;
     const int n_hg = (a.hkv + HW - 1) / HW;
-    const Group g = plan.g[plan_search<&Group::merge_base>(plan, blockIdx.x)];
+    const Group g = group_of<true>(plan, blockIdx.x);
     if (g.n_split <= 1) return;
     const int qh = ((int)blockIdx.x - g.merge_base) * kMergeRows + (int)threadIdx.x / TPR;
     const int q4 = (int)threadIdx.x % TPR;
@@ -1353,8 +1377,7 @@ __global__ void __launch_bounds__(64) attn_f32(const Plan plan, const Args a) {
     constexpr int HALF = D / 2;
     const int lane = threadIdx.x;
     const int bid = blockIdx.x;
-    int unused;
-    const Group g = plan.g[find_group(plan, bid, unused)];
+    const Group g = group_of<false>(plan, bid);
     const int li = bid - g.item_base;
     if (li >= g.n_tok * a.hq) return;
     const int toff = li / a.hq, h = li - toff * a.hq;
@@ -1538,6 +1561,12 @@ int launch_rope_rotate(int dtype, int style, int d, int rot_half, const RopeStep
             hipLaunchKernelGGL((rope_rotate_kernel<__bf16, 1>), grid, dim3(256), 0, st, static_cast<__bf16*>(x),
                                n_pairs, heads, d, rot_half, steps, positions, t, rope_len);
     }
+    return hipGetLastError();
+}
+
+int launch_plan_upload(const PlanUpload& up, void* stream) {
+    if (up.n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(plan_upload_kernel, dim3((unsigned)up.n), dim3(256), 0, (hipStream_t)stream, up);
     return hipGetLastError();
 }
 

@@ -70,3 +70,117 @@ def rope_variant_case(dtype, D=128, rotary_dim=None, inv_freq=None, decode=False
     wl.rotary_dim = rotary_dim
     wl.rope_inv_freq = inv_freq
     return wl
+
+
+def many_spans_prefill(dtype=torch.bfloat16, seed=60):
+    """More query spans than the kernel arguments hold (82 groups, so the group table
+    goes through the workspace in two upload launches): 26 requests of three query
+    spans over a shared cached prefix, and 4 requests whose query tail sees 1024
+    cached keys (long enough to be split, so the split merge reads the table too)."""
+    rng = np.random.default_rng(seed)
+    reqs = []
+    for r in range(26):
+        n1, n2, n3 = (int(x) for x in rng.integers(1, 70, size=3))
+        reqs.append([Sp(32, S, key="pre"), Sp(n1, S | Q, fresh=True), Sp(n2, Q, fresh=True),
+                     Sp(n3, Pd | Q, fresh=True)])
+    for r in range(4):
+        reqs.append([Sp(1024, S, key="long"), Sp(int(rng.integers(20, 90)), Pd | Q, fresh=True)])
+    return W.small_case("many_spans", reqs, Hq=8, Hkv=2, D=128, theta=5e5, dtype=dtype, seed=seed,
+                        value_scale=0.5)
+
+
+def many_requests_decode(num_reqs=256, Hq=32, Hkv=8, D=128, seed=61):
+    """256 decode requests of 1 to ~600 tokens (more groups than the kernel
+    arguments hold; the longer ones are split, the shorter are not)."""
+    rng = np.random.default_rng(seed)
+    reqs = []
+    for r in range(num_reqs):
+        kind = r % 4
+        if kind == 0:
+            spans = [Sp(int(rng.integers(1, 40)), Pd, fresh=True)]
+        elif kind == 1:
+            spans = [Sp(64, S, key="a"), Sp(int(rng.integers(1, 200)), S), Sp(1, 0, fresh=True)]
+        elif kind == 2:
+            spans = [Sp(128, S, key="b"), Sp(64, S, key="a"), Sp(int(rng.integers(100, 400)), Pd), Sp(1, Pd, fresh=True)]
+        else:
+            spans = [Sp(int(rng.integers(16, 80)), S), Sp(1, S, fresh=True)]
+        reqs.append(spans)
+    return W.small_case("many_requests_decode", reqs, Hq=Hq, Hkv=Hkv, D=D, theta=5e5, dtype=torch.bfloat16,
+                        seed=seed, value_scale=0.5, decode=True,
+                        position_offsets=[int(x) for x in rng.integers(0, 5000, size=num_reqs)])
+
+
+# ---- peaked scores: the running maximum of the online softmax must move -------------------
+
+LOG2E = 1.4426950408889634
+PEAK_SCALE = 0.125 / LOG2E   # softmax scale whose log2-domain factor is 1/8 exactly
+
+
+def plant_rising_keys(wl, every=64, offset=37, q_val=4.0, a_max=250.0):
+    """Make later keys dominate: every `every`-th key (sequence index = offset mod
+    `every`) of every request gets amplitude A(j) = 16 .. a_max, growing with its
+    sequence index j, on the lowest-frequency RoPE pair (NeoX dims D/2-1 and D-1,
+    which turn by less than a milliradian over these positions), and every query
+    gets q_val on the same pair.  With softmax_scale = PEAK_SCALE a planted key's
+    score is q_val * A / 8 in log2 units plus the small random part of the other
+    dims, so along the sequence the row maximum rises by several times the kernels'
+    rescale threshold and the output is a mix of the last few planted values (O(1)
+    entries).  Values are exact in bf16 (even integers below 256)."""
+    D = wl.head_dim
+    lo, hi = D // 2 - 1, D - 1
+    fresh_row = {(int(r), int(t)): i for i, (r, t) in enumerate(wl.info["fresh_tokens"])}
+    for r in range(wl.num_reqs):
+        L = int(wl.seq_lens[r])
+        for j in range(offset, L, every):
+            a = float(2 * round((16.0 + (a_max - 16.0) * j / max(L - 1, 1)) / 2))
+            if (r, j) in fresh_row:
+                i = fresh_row[(r, j)]
+                wl.k_new[i, :, lo] = a
+                wl.k_new[i, :, hi] = 0.0
+            else:
+                b = int(wl.block_tables[r, j // 16])
+                wl.k_pool[b, :, j % 16, lo] = a
+                wl.k_pool[b, :, j % 16, hi] = 0.0
+    wl.q[:, :, lo] = q_val
+    wl.q[:, :, hi] = 0.0
+    wl.softmax_scale = PEAK_SCALE
+    return wl
+
+
+def rise_of_max(wl, rows=None):
+    """Premise check in fp64 (oracle RoPE): for each query row t and head h, the
+    maximum log2-domain score over its visible keys after the first 64 minus the
+    maximum over the first 64 (NaN for rows seeing at most 64 keys).  A value above 8
+    means the kernels' running maximum has to move after their first key tile."""
+    import math
+    from oracle import pic_oracle as O
+    from oracle import workload_oracle as WO
+    k, _ = WO.pools_after_write(wl)
+    q = wl.q.double().numpy()
+    G = wl.num_q_heads // wl.num_kv_heads
+    scale = (wl.softmax_scale or 1.0 / math.sqrt(wl.head_dim)) * LOG2E
+    out = []
+    row = 0
+    for r in range(wl.num_reqs):
+        L = int(wl.seq_lens[r])
+        sl = slice(wl.cu_spans[r], wl.cu_spans[r + 1])
+        w = O.span_windows(wl.span_start[sl], wl.span_flags[sl], L, None)
+        qi = np.array([L - 1]) if wl.is_decode else O.query_tokens(wl.span_start[sl], wl.span_flags[sl], L)
+        pos = wl.positions[wl.seq_offsets[r]:wl.seq_offsets[r] + L].astype(np.int64)
+        n = np.arange(L)
+        K = O.rope(k[wl.block_tables[r][n // 16], :, n % 16, :], pos[:, None], wl.rope_theta)
+        sel = np.arange(len(qi)) if rows is None else np.array([i for i in range(len(qi)) if row + i in rows], int)
+        if len(sel):
+            t = qi[sel]
+            lo, first_end = w[t], w[t] + 64
+            j = np.arange(L)[None, :]
+            early = (j >= lo[:, None]) & (j < first_end[:, None]) & (j <= t[:, None])
+            late = (j >= first_end[:, None]) & (j <= t[:, None])
+            qr = O.rope(q[row + sel], pos[t][:, None], wl.rope_theta)       # [n][Hq][D]
+            for h in range(wl.num_q_heads):
+                s = qr[:, h, :] @ K[:, h // G, :].T * scale                 # [n][L]
+                m1 = np.where(early, s, -np.inf).max(axis=1)
+                m2 = np.where(late, s, -np.inf).max(axis=1)
+                out.append(np.where(np.isfinite(m2), m2 - m1, np.nan))
+        row += len(qi)
+    return np.concatenate(out) if out else np.array([])

@@ -11,3 +11,25 @@ if ROOT not in sys.path:
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU")
     config.addinivalue_line("markers", "slow: long-running CPU test")
+
+
+def pytest_terminal_summary(terminalreporter):
+    """Print every GPU-vs-reference comparison of the run (max-abs, relative L2 and
+    the largest reference entry, which shows whether max-abs binds) and keep a copy
+    in gpurun_out/parity_summary.txt when that folder exists."""
+    try:
+        from tests.gpu_util import RECORDS
+    except Exception:  # pragma: no cover
+        return
+    if not RECORDS:
+        return
+    lines = [f"{'comparison':64s} {'dtype':5s} {'max_abs':>10s} {'rel_l2':>10s} {'max|ref|':>9s}"]
+    for what, ma, rel, peak, dt in RECORDS:
+        lines.append(f"{what[:64]:64s} {dt:5s} {ma:10.3e} {rel:10.3e} {peak:9.3g}")
+    terminalreporter.write_line("parity records (GPU vs oracle or vs another GPU path):")
+    for ln in lines:
+        terminalreporter.write_line(ln)
+    out = os.path.join(ROOT, "gpurun_out")
+    if os.path.isdir(out):
+        with open(os.path.join(out, "parity_summary.txt"), "w") as f:
+            f.write("\n".join(lines) + "\n")

@@ -12,6 +12,10 @@ from oracle import workload_oracle as WO
 BF16_MAX_ABS, BF16_REL_L2 = 2e-2, 5e-3
 F32_MAX_ABS = 1e-4
 
+# every comparison of the session: (what, max_abs, rel_l2, max |reference|), printed
+# as a table at the end of the run (tests/conftest.py)
+RECORDS = []
+
 
 def say(*a):
     print(*a, flush=True)
@@ -46,7 +50,9 @@ def errors(got, ref):
 def assert_close(got, ref, dtype, what=""):
     assert np.all(np.isfinite(got)), f"{what}: non-finite output"
     max_abs, rel = errors(got, ref)
-    say(f"  {what}: max_abs={max_abs:.3e} rel_l2={rel:.3e}")
+    peak = float(np.max(np.abs(ref))) if np.size(ref) else 0.0
+    RECORDS.append((what, max_abs, rel, peak, "fp32" if dtype == torch.float32 else "bf16"))
+    say(f"  {what}: max_abs={max_abs:.3e} rel_l2={rel:.3e} max|ref|={peak:.3g}")
     if dtype == torch.float32:
         assert max_abs <= F32_MAX_ABS, (what, max_abs)
     else:

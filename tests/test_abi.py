@@ -271,3 +271,42 @@ def test_plan_exact_cover_explicit_windows(dtype):
     wl = windows_prefill_case()
     assert check_exact_cover(wl, dtype, False) == (16 + 16 + 40 + 37) * 8
     assert check_exact_cover(windows_decode_case(), dtype, True) == 2 * 32
+
+
+# ---- batches with more groups than the kernel arguments hold ----------------------------
+
+@pytest.mark.parametrize("dtype", [B.PIC_BF16, B.PIC_F32])
+def test_plan_exact_cover_many_spans(dtype):
+    from tests.cases import many_spans_prefill
+    wl = many_spans_prefill()
+    n = check_exact_cover(wl, dtype, False)
+    assert n == wl.q.shape[0] * wl.num_q_heads
+    cfg = P.make_config(wl.num_q_heads, wl.num_kv_heads, wl.head_dim, dtype=dtype)
+    shape = P.pic_plan_shape(cfg, batch_of(wl), False)
+    assert shape["groups"] == 82 and shape["upload_launches"] == 2
+    if dtype == B.PIC_BF16:
+        assert shape["merge_blocks"] > 0 and shape["partial_slots"] > 0   # the long tails are split
+    # the workspace holds the group table and block maps besides the partials
+    ws = P.pic_workspace_size(cfg, batch_of(wl), False)
+    parts = shape["partial_slots"] * 256 * (wl.head_dim + 2) * 4
+    assert ws >= parts + 82 * 48 + 4 * (shape["attention_blocks"] + shape["merge_blocks"])
+
+
+@pytest.mark.parametrize("Hq,Hkv,D", [(32, 8, 128), (34, 2, 64)])
+def test_plan_exact_cover_many_requests_decode(Hq, Hkv, D):
+    from tests.cases import many_requests_decode
+    wl = many_requests_decode(Hq=Hq, Hkv=Hkv, D=D)
+    assert check_exact_cover(wl, B.PIC_BF16, True) == 256 * Hq
+    cfg = P.make_config(Hq, Hkv, D)
+    shape = P.pic_plan_shape(cfg, batch_of(wl), True)
+    assert shape["groups"] == 256 and shape["upload_launches"] == 4
+
+
+def test_decode_256_requests_is_one_launch_filling_the_chip():
+    # 256 requests of 8193 keys: one attention launch of at least 256 workgroups (one
+    # per request and head group), not a series of launches over slices of the batch
+    wl = W.decode_64req(num_reqs=256, num_spans=4, span_len=512)
+    cfg = P.make_config(32, 8, 128)
+    shape = P.pic_plan_shape(cfg, batch_of(wl), True)
+    assert shape["groups"] == 256 and shape["attention_blocks"] >= 256
+    assert shape["upload_launches"] == 4

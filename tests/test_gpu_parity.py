@@ -6,7 +6,8 @@ import torch
 import workloads as W
 from oracle import pic_oracle as O
 from oracle import workload_oracle as WO
-from tests.cases import decode_case, windows_decode_case, windows_prefill_case
+from tests.cases import (decode_case, many_requests_decode, many_spans_prefill, plant_rising_keys, rise_of_max,
+                         windows_decode_case, windows_prefill_case)
 from tests.gpu_util import assert_close, gpu_run, say, to_np
 
 pytestmark = pytest.mark.gpu
@@ -62,12 +63,9 @@ def test_decode_64req_bf16():
     check(W.decode_64req())
 
 
-def test_llama3_70b_long_sampled_rows():
-    wl = W.llama3_70b_long()
-    rng = np.random.default_rng(4)
-    n = wl.q.shape[0]
-    rows = np.unique(np.concatenate([rng.choice(n, 48, replace=False), [0, n - 1, n - 512, n - 513, 511, 512]]))
-    check(wl, rows=rows)
+def test_llama3_70b_long_all_rows():
+    # the largest workload, every one of its 16,896 query tokens x 64 heads
+    check(W.llama3_70b_long())
 
 
 @pytest.mark.parametrize("style", [0, 1])
@@ -318,3 +316,97 @@ def test_generalised_windows_prefill(dtype):
 
 def test_generalised_windows_decode():
     check(windows_decode_case(), what="generalised windows decode")
+
+
+# ---- more groups than the kernel arguments hold: the group table goes through the
+# workspace (written by plan-upload launches), one attention and one merge launch ----
+
+def shape_of(wl, dtype=None):
+    import paper_2606_13126_amd as P
+    from paper_2606_13126_amd.runner import config_of
+    cfg = config_of(wl)
+    return P.pic_plan_shape(cfg, P.HostBatch(wl.seq_lens, wl.cu_spans, wl.span_start, wl.span_flags,
+                                             wl.span_window), wl.is_decode)
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_many_query_spans_prefill(dtype):
+    wl = many_spans_prefill(dtype)
+    sh = shape_of(wl)
+    say(f"[gpu] many spans {dtype}: {sh}")
+    assert sh["groups"] == 82 and sh["upload_launches"] == 2
+    if dtype == torch.bfloat16:
+        assert sh["merge_blocks"] > 0
+    check(wl, what=f"82 query spans {dtype}")
+
+
+@pytest.mark.parametrize("Hq,Hkv,D,style", [(32, 8, 128, 0), (34, 2, 64, 1)])
+def test_many_requests_decode(Hq, Hkv, D, style):
+    wl = many_requests_decode(Hq=Hq, Hkv=Hkv, D=D)
+    sh = shape_of(wl)
+    say(f"[gpu] 256-request decode Hq={Hq} Hkv={Hkv} D={D}: {sh}")
+    assert sh["groups"] == 256 and sh["upload_launches"] == 4
+    check(wl, style=style, what=f"256-request decode Hq={Hq} D={D}")
+
+
+def test_many_requests_decode_fp32():
+    wl = many_requests_decode(Hq=8, Hkv=2, D=128)
+    wl.dtype = torch.float32
+    for name in ("q", "k_pool", "v_pool", "k_new", "v_new"):
+        setattr(wl, name, getattr(wl, name).float())
+    check(wl, what="256-request decode fp32")
+
+
+# ---- peaked scores: keys whose alignment with the queries grows along the sequence, so
+# the online softmax's running maximum rises by far more than its rescale threshold
+# after the first key tile, in unsplit and split prefill, decode and the fp32 path ----
+
+def check_peaked(wl, expect_split, min_frac, style=0, rows=None):
+    plant_rising_keys(wl)
+    rise = rise_of_max(wl, rows=None if rows is None else set(int(x) for x in rows))
+    frac = float(np.nanmean(rise > 8)) if np.any(~np.isnan(rise)) else 0.0
+    sh = shape_of(wl)
+    say(f"[gpu] peaked {wl.name}: rows whose max rises by >8 (log2) after the first tile: {frac:.2f}, "
+        f"largest rise {np.nanmax(rise):.1f}; plan {sh}")
+    assert frac >= min_frac, frac
+    if expect_split is not None and wl.dtype == torch.bfloat16:
+        assert (sh["partial_slots"] > 0) == expect_split, sh
+    max_abs, _ = check(wl, style=style, rows=rows, what=f"peaked {wl.name}")
+    return max_abs
+
+
+def test_peaked_prefill_unsplit():
+    # 16 requests x 2 row tiles x 8 KV heads fill the chip without key splits
+    check_peaked(W.concurrent_reuse(), expect_split=False, min_frac=0.9)
+
+
+def test_peaked_prefill_split_small():
+    wl = W.small_case("peak_small", [[Sp(64, S, key="a"), Sp(300, S | Q, fresh=True), Sp(200, Pd | Q, fresh=True)]],
+                      Hq=4, Hkv=2, D=128, theta=5e5, dtype=torch.bfloat16, seed=3, value_scale=0.5)
+    check_peaked(wl, expect_split=True, min_frac=0.5)
+
+
+def test_peaked_llama3_8b_rag_split():
+    # 8 key splits per row tile: every split's running maximum moves, and the merge
+    # combines splits whose maxima differ by up to ~100 (log2)
+    check_peaked(W.llama3_8b_rag(), expect_split=True, min_frac=0.9)
+
+
+def test_peaked_decode():
+    check_peaked(W.decode_64req(num_reqs=16), expect_split=True, min_frac=0.8)
+
+
+def test_peaked_decode_mixed_windows():
+    check_peaked(decode_case(32, 8, 128, seed=71), expect_split=None, min_frac=0.4)
+
+
+def test_peaked_tiny_fp32():
+    check_peaked(W.tiny_fp32(), expect_split=None, min_frac=0.15)
+
+
+def test_peaked_decode_fp32():
+    wl = decode_case(8, 2, 128, seed=72)
+    wl.dtype = torch.float32
+    for name in ("q", "k_pool", "v_pool", "k_new", "v_new"):
+        setattr(wl, name, getattr(wl, name).float())
+    check_peaked(wl, expect_split=None, min_frac=0.4)
