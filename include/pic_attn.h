@@ -210,6 +210,20 @@ pic_status pic_attn_decode(const pic_config* cfg, const pic_batch_host* batch, c
                            const void* v_pool, int32_t num_blocks, void* workspace, size_t workspace_bytes,
                            void* stream);
 
+/* pic_attn_decode for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * arguments minus the workspace, the same kernels and results.  The split-KV
+ * partials and the group table live in a 64 MiB device scratch array inside the
+ * library, one per GPU the library runs on, held until the process ends; the call
+ * allocates nothing.  A batch needing more scratch than that is refused with
+ * PIC_EWORKSPACE before anything is launched (pic_workspace_size(cfg, batch, 1)
+ * gives the need).  Every call on one GPU shares that GPU's scratch: calls that
+ * overlap on one GPU (concurrent streams, or from several threads) race and must
+ * be serialised by the caller.  The stream must belong to the current device. */
+pic_status pic_attn_decode_noalloc(const pic_config* cfg, const pic_batch_host* batch, const pic_batch_dev* dev,
+                                   const pic_rope_table* rope, const void* q, void* o, const void* k_pool,
+                                   const void* v_pool, int32_t num_blocks, void* stream);
+
 /* Test hook: the work decomposition the prefill/decode call would launch, as
  * rows of 8 int32 {request, kv_head, first query row (flattened token*G+head
  * offset within the span), end query row, key begin, key end, span first token,

@@ -7,7 +7,7 @@ package alone does not load it, so ``python -m paper_2606_13126_amd.build`` work
 before the library exists); a missing or broken library raises ImportError.
 """
 _EXPORTS = ("PIC_BF16", "PIC_F32", "PIC_PDEP", "PIC_QUERY", "PIC_ROPE_GPTJ", "PIC_ROPE_NEOX", "PIC_SSEP",
-            "HostBatch", "PicError", "make_config", "pic_attn_decode", "pic_attn_prefill", "pic_kv_write",
+            "HostBatch", "PicError", "make_config", "pic_attn_decode", "pic_attn_decode_noalloc", "pic_attn_prefill", "pic_kv_write",
             "pic_plan_debug", "pic_plan_shape", "pic_rope_rotate", "pic_rope_table_build", "pic_rope_table_bytes", "pic_version",
             "pic_workspace_size", "pic_sha256", "pic_block_hashes", "pic_spans_from_blocks",
             "pic_block_cache_create", "pic_block_cache_destroy", "pic_block_cache_lookup", "pic_block_cache_insert",

@@ -74,6 +74,8 @@ _sig = {
                                   c_void_p, c_void_p, c_void_p, c_void_p, c_int32, c_void_p, c_size_t, c_void_p]),
     "pic_plan_debug": (c_int32, [_P(pic_config), _P(pic_batch_host), c_int32, _P(c_int32), c_int32, _P(c_int32)]),
     "pic_plan_shape": (c_int32, [_P(pic_config), _P(pic_batch_host), c_int32, _P(c_int32)]),
+    "pic_attn_decode_noalloc": (c_int32, [_P(pic_config), _P(pic_batch_host), _P(pic_batch_dev), _P(pic_rope_table),
+                                          c_void_p, c_void_p, c_void_p, c_void_p, c_int32, c_void_p]),
     # span cache (include/pic_cache.h): host only
     "pic_sha256": (c_int32, [c_void_p, c_size_t, c_void_p]),
     "pic_block_hashes": (c_int32, [c_void_p, c_int32, c_int32, c_int32, c_void_p, c_void_p]),
@@ -218,6 +220,15 @@ def pic_attn_decode(cfg: pic_config, batch: HostBatch, block_tables, positions, 
     _check(_lib.pic_attn_decode(ctypes.byref(cfg), ctypes.byref(batch.c), ctypes.byref(_dev(block_tables, positions)),
                                 ctypes.byref(_rope(table)), _ptr(q), _ptr(o), _ptr(k_pool), _ptr(v_pool),
                                 int(k_pool.shape[0]), _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def pic_attn_decode_noalloc(cfg: pic_config, batch: HostBatch, block_tables, positions, q, o, k_pool, v_pool,
+                            table=None, stream=None) -> None:
+    """pic_attn_decode without a workspace (the library's device scratch holds the partials)."""
+    _check(_lib.pic_attn_decode_noalloc(ctypes.byref(cfg), ctypes.byref(batch.c),
+                                        ctypes.byref(_dev(block_tables, positions)), ctypes.byref(_rope(table)),
+                                        _ptr(q), _ptr(o), _ptr(k_pool), _ptr(v_pool), int(k_pool.shape[0]),
+                                        _stream(stream)))
 
 
 def pic_plan_debug(cfg: pic_config, batch: HostBatch, is_decode: bool) -> np.ndarray:

@@ -587,6 +587,24 @@ pic_status pic_attn_decode(const pic_config* cfg, const pic_batch_host* batch, c
                          true);
 }
 
+pic_status pic_attn_decode_noalloc(const pic_config* cfg, const pic_batch_host* batch, const pic_batch_dev* dev,
+                                   const pic_rope_table* rope, const void* q, void* o, const void* k_pool,
+                                   const void* v_pool, int32_t num_blocks, void* stream) {
+    pic_status st = check_config(cfg);
+    if (st) return st;
+    if ((st = check_batch(batch))) return st;
+    HostPlan hp;
+    if ((st = build_plan(cfg, batch, true, hp))) return st;
+    const size_t need = ws_layout(cfg, hp).total;
+    if (need > pic::kScratchBytes)
+        return fail(PIC_EWORKSPACE, "batch needs " + std::to_string(need) + " bytes of scratch; the no-allocation "
+                    "entry point has " + std::to_string(pic::kScratchBytes) + " (use pic_attn_decode with a workspace)");
+    void* ws = nullptr;
+    if ((st = hip_status(pic::scratch_region(&ws), "scratch address"))) return st;
+    return run_attention(cfg, batch, dev, rope, q, o, k_pool, v_pool, num_blocks, ws, pic::kScratchBytes, stream,
+                         true);
+}
+
 pic_status pic_plan_debug(const pic_config* cfg, const pic_batch_host* batch, int32_t is_decode, int32_t* items,
                           int32_t capacity, int32_t* n_items) {
     pic_status st = check_config(cfg);

@@ -139,4 +139,11 @@ int launch_attention(int dtype, int style, int d, bool rope, const Plan& plan, c
 int launch_decode(int style, int d, bool rope, const Plan& plan, const Args& args, void* stream);
 int launch_plan_upload(const PlanUpload& up, void* stream);
 
+// Device scratch of the no-allocation entry point: kScratchBytes on each device,
+// shared by every call on that device.  scratch_region returns the current
+// device's address of it (a hipError_t value).
+constexpr size_t kScratchBytes = (size_t)64 << 20;
+constexpr int kMaxDevices = 64;
+int scratch_region(void** ptr);
+
 }  // namespace pic

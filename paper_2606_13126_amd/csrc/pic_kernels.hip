@@ -18,6 +18,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
 #include <type_traits>
 
 #include "pic_internal.h"
@@ -1505,6 +1506,33 @@ hipError_t launch_attn_d(int dtype, bool rope, const Plan& plan, const Args& a, 
 }
 
 }  // namespace
+
+// ---------------------------------------------------------------------------------
+// Scratch for the entry point that allocates nothing (pic_attn_decode_noalloc): a
+// file-scope device array, present on every GPU the library's code is loaded on
+// until the process ends.  Host code must not use the array's name as an address
+// (it is a host-side stand-in): its device address is taken once per device with
+// hipGetSymbolAddress, with that device current, and only that address is passed on.
+// ---------------------------------------------------------------------------------
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+int scratch_region(void** ptr) {
+    static std::mutex mu;
+    static void* addr[kMaxDevices] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (addr[dev] == nullptr) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        addr[dev] = p;
+    }
+    *ptr = addr[dev];
+    return hipSuccess;
+}
 
 int launch_kv_write(int dtype, int hkv, int d, void* k_pool, void* v_pool, const void* k_new, const void* v_new,
                     const int32_t* slots, int n, void* stream) {

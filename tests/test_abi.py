@@ -310,3 +310,24 @@ def test_decode_256_requests_is_one_launch_filling_the_chip():
     shape = P.pic_plan_shape(cfg, batch_of(wl), True)
     assert shape["groups"] == 256 and shape["attention_blocks"] >= 256
     assert shape["upload_launches"] == 4
+
+
+def test_noalloc_decode_refuses_batches_beyond_its_scratch():
+    # 255 requests of 4097 keys: 2 key splits each (510 partial slots), more than the
+    # no-allocation entry point's 64 MiB of scratch.  Refused on the host with
+    # PIC_EWORKSPACE before any HIP call (the pointers are never dereferenced).
+    lib = B.lib()
+    R, L = 255, 4097
+    seq = np.full(R, L, np.int32)
+    cu = np.arange(R + 1, dtype=np.int32)
+    hb = B.HostBatch(seq, cu, np.zeros(R, np.int32), np.full(R, W.PDEP, np.int32))
+    cfg = P.make_config(32, 8, 128, rope_theta=5e5)
+    need = P.pic_workspace_size(cfg, hb, True)
+    assert need > 64 << 20
+    fake = 16
+    dev = B.pic_batch_dev(fake, (L + 15) // 16, fake)
+    rc = lib.pic_attn_decode_noalloc(ctypes.byref(cfg), ctypes.byref(hb.c), ctypes.byref(dev), None, fake, fake, fake,
+                                     fake, 16, None)
+    assert rc == B.PIC_EWORKSPACE
+    msg = lib.pic_last_error().decode()
+    assert "scratch" in msg and str(need) in msg
