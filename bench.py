@@ -3,13 +3,15 @@
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu] [--no-extra]
 
 A step is one pass of the hot path over one synthetic batch of the
-Llama-3-8B-shaped RAG prefill (10 cached 512-token SSEP spans, a fresh 256-token
-PDEP query tail, 32/8 heads, head_dim 128, theta 5e5, bf16): pic_kv_write of the
-tail's K/V rows followed by pic_attn_prefill.  Inputs are resident in HBM before
-the timed region.  ``value`` is the algorithmic prefill work (4*D*Hq per visible
-query/key pair) per step time, in TFLOP/s.  Extra fields time every workload,
-the fused-RoPE overhead against the same kernel on pre-rotated K, the decode
-bandwidth, and the fp64 CPU oracle on this host.
+Llama-3-70B-shaped long prefill (one request of 64 SSEP spans of 512 tokens, a
+seeded half of them fresh and computed in the call, the other half cached, plus a
+fresh 512-token PDEP query tail: 33,280 tokens, 64/8 heads, head_dim 128, theta 5e5,
+bf16): pic_kv_write of the 16,896 fresh K/V rows followed by pic_attn_prefill.
+Inputs are resident in HBM before the timed region.  ``value`` is the algorithmic
+prefill work (4*D*Hq per visible query/key pair, 691.8 GFLOP) per step time, in
+TFLOP/s.  Extra fields time every other workload, the fused-RoPE overhead against
+the same kernel on pre-rotated K, the decode bandwidth, and the fp64 CPU oracle on
+this host.
 """
 from __future__ import annotations
 
@@ -77,9 +79,41 @@ def decode_bytes(wl) -> float:
     return kv + qo + meta
 
 
+def row_pairs(wl) -> np.ndarray:
+    """Visible keys of every query row of a prefill workload (rows in q order)."""
+    out = []
+    for r in range(wl.num_reqs):
+        L = int(wl.seq_lens[r])
+        sl = slice(wl.cu_spans[r], wl.cu_spans[r + 1])
+        st, fl = wl.span_start[sl], wl.span_flags[sl]
+        sw = None if wl.span_window is None else wl.span_window[sl]
+        prev = 0
+        for k in range(len(st)):
+            b, e = int(st[k]), (int(st[k + 1]) if k + 1 < len(st) else L)
+            f = int(fl[k])
+            w = b if f & W.SSEP else (0 if f & W.PDEP else prev)
+            if sw is not None and int(sw[k]) >= 0:
+                w = int(sw[k])
+            prev = w
+            if f & W.QUERY:
+                out.append(np.arange(b, e, dtype=np.int64) - w + 1)
+    return np.concatenate(out) if out else np.zeros(0, np.int64)
+
+
+def unique_kv_bytes(wl) -> float:
+    """K+V bytes of the distinct physical blocks a decode batch reads."""
+    esize = 2 if wl.dtype == torch.bfloat16 else 4
+    blocks = set()
+    for r in range(wl.num_reqs):
+        nb = (int(wl.seq_lens[r]) + 15) // 16
+        blocks.update(int(b) for b in wl.block_tables[r, :nb])
+    return float(len(blocks)) * wl.num_kv_heads * 16 * wl.head_dim * 2 * esize
+
+
+HEADLINE = "llama3_70b_long"
 KERNEL_SOURCES = ("paper_2606_13126_amd/csrc/pic_kernels.hip", "paper_2606_13126_amd/csrc/pic_host.cpp",
                   "paper_2606_13126_amd/csrc/pic_internal.h")
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_prefill_llama3_8b_rag.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_prefill_llama3_70b_long.json")
 
 
 def kernel_source_hash() -> str:
@@ -141,11 +175,17 @@ def bench_workload(wl, steps, warmup, stream, with_control=True):
     out["attn_ms_median"] = float(np.median(ms))
     out["attn_ms_p10"] = float(np.percentile(ms, 10))
     out["attn_ms_p90"] = float(np.percentile(ms, 90))
+    if wl.k_new.shape[0]:
+        out["kv_write_ms_median"] = float(np.median(timed(db.write, steps, warmup, stream)))
+        out["kv_write_rows"] = int(wl.k_new.shape[0])
     if wl.is_decode:
-        gbs = decode_bytes(wl) / (out["attn_ms_median"] * 1e-3) / 1e9
-        out["decode_GBps"] = gbs
-        out["pct_hbm_peak"] = 100.0 * gbs / PEAK_HBM_GBS
+        algo = decode_bytes(wl)
+        uniq = unique_kv_bytes(wl)
+        kv = float(np.sum(wl.seq_lens)) * wl.num_kv_heads * wl.head_dim * 2 * (2 if wl.dtype == torch.bfloat16 else 4)
+        out["algorithmic_bytes"] = algo
+        out["unique_kv_bytes"] = uniq
         out["tokens_per_s"] = wl.num_reqs / (out["attn_ms_median"] * 1e-3)
+        gbs = algo / (out["attn_ms_median"] * 1e-3) / 1e9
         # cold: a 1 GiB write between calls evicts the K/V from the 256 MB Infinity Cache
         scratch = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
         cold = []
@@ -159,7 +199,17 @@ def bench_workload(wl, steps, warmup, stream, with_control=True):
             cold.append(a.elapsed_time(b))
         del scratch
         out["attn_ms_cold_median"] = float(np.median(cold))
-        out["decode_GBps_cold"] = decode_bytes(wl) / (out["attn_ms_cold_median"] * 1e-3) / 1e9
+        gbs_cold = algo / (out["attn_ms_cold_median"] * 1e-3) / 1e9
+        if uniq < 0.99 * kv:
+            # shared spans: the same blocks are read by many requests, largely from the
+            # Infinity Cache, so bytes per second of the algorithm are not HBM bandwidth
+            out["effective_GBps"] = gbs
+            out["effective_GBps_cold"] = gbs_cold
+        else:
+            out["decode_GBps"] = gbs
+            out["pct_hbm_peak"] = 100.0 * gbs / PEAK_HBM_GBS
+            out["decode_GBps_cold"] = gbs_cold
+            out["pct_hbm_peak_cold"] = 100.0 * gbs_cold / PEAK_HBM_GBS
     else:
         tf = flops_of(wl) / (out["attn_ms_median"] * 1e-3) / 1e12
         out["TFLOPs"] = tf
@@ -217,8 +267,10 @@ def bench_offload(steps, stream, n_blocks=4096, hkv=8, d=128):
     return out
 
 
-def cpu_baseline(wl, budget_s=12.0):
-    """The fp64 oracle (kv_write + prefill) on this host, repeated for about budget_s."""
+def cpu_baseline(wl, fraction=0.25, seed=0):
+    """The fp64 oracle on this host: kv_write of the whole workload and the prefill of
+    a seeded sample of its query rows (``fraction`` of them), timed once; the rate is
+    the sample's own algorithmic work over that time."""
     from oracle import workload_oracle as WO
     try:
         from threadpoolctl import threadpool_info
@@ -226,18 +278,17 @@ def cpu_baseline(wl, budget_s=12.0):
     except Exception:  # pragma: no cover
         blas = None
     cores = len(os.sched_getaffinity(0))
-    runs, t0 = 0, time.perf_counter()
-    while True:
-        WO.run(wl)
-        runs += 1
-        el = time.perf_counter() - t0
-        if el >= budget_s or runs >= 500:
-            break
-    per = el / runs
-    return {"value": flops_of(wl) / per / 1e12, "unit": "TFLOP/s", "cores": int(blas or cores),
-            "kind": "oracle", "host_cores": cores,
-            "sample": f"whole workload (kv_write + prefill of {wl.q.shape[0]} query tokens x {wl.num_q_heads} heads), "
-                      f"{runs} run(s), {per:.3f} s each, fp64 NumPy"}
+    n = wl.q.shape[0]
+    rows = np.sort(np.random.default_rng(seed).choice(n, size=max(1, int(round(fraction * n))), replace=False))
+    work = 4.0 * wl.head_dim * wl.num_q_heads * float(row_pairs(wl)[rows].sum())
+    t0 = time.perf_counter()
+    WO.run(wl, rows=rows)
+    el = time.perf_counter() - t0
+    return {"value": work / el / 1e12, "unit": "TFLOP/s", "cores": int(blas or cores), "kind": "oracle",
+            "host_cores": cores,
+            "sample": f"{wl.name}: kv_write of all {wl.k_new.shape[0]} fresh rows + prefill of {len(rows)} of its "
+                      f"{n} query tokens (seeded {fraction:.0%} sample) x {wl.num_q_heads} heads, "
+                      f"{work / 1e9:.1f} GFLOP in {el:.2f} s, fp64 NumPy"}
 
 
 def main():
@@ -247,8 +298,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-extra", action="store_true")
-    ap.add_argument("--workloads", default="concurrent_reuse,decode_64req,decode_64req_unshared,llama3_70b_long",
-                    help="extra workloads (names of workloads.WORKLOADS, or decode_64req_unshared)")
+    ap.add_argument("--workloads", default="llama3_70b_long,llama3_8b_rag,concurrent_reuse,decode_64req,"
+                                           "decode_64req_unshared,decode_256req_unshared",
+                    help="extra workloads (names of workloads.WORKLOADS, decode_64req_unshared or "
+                         "decode_256req_unshared)")
     ap.add_argument("--no-offload", action="store_true")
     ap.add_argument("--calib", action="store_true", help="also run the 256 MiB calibration copy")
     args = ap.parse_args()
@@ -262,7 +315,7 @@ def main():
     from paper_2606_13126_amd.runner import DeviceBatch
     stream = torch.cuda.current_stream()
 
-    wl = W.llama3_8b_rag()
+    wl = W.make(HEADLINE)
     flops = flops_of(wl)
     db = DeviceBatch(wl, table_positions=table_len(wl))
 
@@ -289,25 +342,33 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": "llama3_8b_rag_prefill: 1 request, 10 cached SSEP spans x 512 + fresh 256-token "
-                               "PDEP query tail (5376 tokens), 32 q / 8 kv heads, head_dim 128, theta 5e5, "
-                               "block 16, bf16",
-                   "step": "pic_kv_write(256 rows) + pic_attn_prefill"},
+        "config": {"workload": "llama3_70b_long_prefill: 1 request of 64 SSEP spans x 512 tokens (32 fresh and "
+                               "queried, 32 cached) + fresh 512-token PDEP query tail (33,280 tokens, 16,896 "
+                               "queries), 64 q / 8 kv heads, head_dim 128, theta 5e5, block 16, bf16",
+                   "step": "pic_kv_write(16,896 rows) + pic_attn_prefill"},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_BF16_TFLOPS, "traffic": measured_traffic(),
-                     "kernel": "pic_attn_prefill call (prefill_bf16 + split merge)", "avg_ms": attn_avg},
+                     "kernel": "pic_attn_prefill call (prefill_bf16 + split merge)", "avg_ms": attn_avg,
+                     "flops_per_call": flops},
     }
     del db
     torch.cuda.empty_cache()
     if args.calib:
         calibration_copy()
     if not args.no_extra:
-        extra = {"llama3_8b_rag": bench_workload(wl, args.steps, args.warmup, stream)}
+        extra = {}
         for name in [x.strip() for x in args.workloads.split(",") if x.strip()]:
-            # decode_64req_unshared: the decode workload with every request's spans
-            # private (2.15 GB of unique K/V, the HBM-bound control of the shared-span decode)
-            w = W.decode_64req(shared=False) if name == "decode_64req_unshared" else W.make(name)
-            extra[name] = bench_workload(w, max(args.steps // 2, 10), max(args.warmup // 2, 3), stream)
+            # decode_*_unshared: every request owns its spans (2.15 GB of unique K/V), the
+            # HBM-bound control of the shared-span decode
+            if name == "decode_64req_unshared":
+                w = W.decode_64req(shared=False)
+            elif name == "decode_256req_unshared":
+                w = W.decode_64req(num_reqs=256, num_spans=4, shared=False)
+            else:
+                w = W.make(name)
+            steps, warm = (args.steps, args.warmup) if name == HEADLINE else (max(args.steps // 2, 10),
+                                                                            max(args.warmup // 2, 3))
+            extra[name] = bench_workload(w, steps, warm, stream)
             print(f"# {name}: {json.dumps(extra[name])}", file=sys.stderr, flush=True)
             del w
             torch.cuda.empty_cache()

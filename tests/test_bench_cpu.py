@@ -54,7 +54,29 @@ def test_more_than_one_gpu_is_refused():
     assert r.returncode == 2 and "one GPU" in r.stderr
 
 
+def test_flops_and_row_pairs_of_the_70b_long_prefill():
+    # 32 fresh SSEP spans of 512 tokens (each token t of a span sees t+1 keys of its
+    # own span) and a 512-token PDEP tail after 32,768 tokens: 21,111,040 pairs
+    wl = W.llama3_70b_long()
+    fresh = 32 * sum(range(1, 513))
+    tail = sum(32768 + t + 1 for t in range(512))
+    assert fresh == 4202496 and tail == 16908544
+    assert bench.flops_of(wl) == 4.0 * 128 * 64 * (fresh + tail) == oracle_flops(wl)
+    rp = bench.row_pairs(wl)
+    assert rp.shape == (wl.q.shape[0],) and int(rp.sum()) == fresh + tail
+
+
+def test_unique_kv_bytes_shared_and_unshared_decode():
+    page = 8 * 16 * 128 * 2 * 2
+    assert bench.unique_kv_bytes(W.decode_64req()) == (16 * 32 + 64) * page    # 16 shared spans + 64 private blocks
+    un = W.decode_64req(num_reqs=8, num_spans=4, shared=False)
+    assert bench.unique_kv_bytes(un) == 8 * (4 * 32 + 1) * page
+
+
 def test_traffic_is_reported_only_for_the_measured_sources(monkeypatch):
+    if not os.path.exists(bench.TRAFFIC_FILE):
+        assert bench.measured_traffic() is None
+        pytest.skip("no counter summary for the headline workload yet")
     with open(bench.TRAFFIC_FILE) as f:
         t = json.load(f)
     monkeypatch.setattr(bench, "kernel_source_hash", lambda: t["source_hash"])
