@@ -267,9 +267,25 @@ def bench_offload(steps, stream, n_blocks=4096, hkv=8, d=128):
     return out
 
 
+def query_span_rows(wl):
+    """(first row, end row) in q of every query span of a prefill workload."""
+    out, row = [], 0
+    for r in range(wl.num_reqs):
+        L = int(wl.seq_lens[r])
+        sl = slice(wl.cu_spans[r], wl.cu_spans[r + 1])
+        st, fl = wl.span_start[sl], wl.span_flags[sl]
+        for k in range(len(st)):
+            if int(fl[k]) & W.QUERY:
+                e = int(st[k + 1]) if k + 1 < len(st) else L
+                out.append((row, row + e - int(st[k])))
+                row += e - int(st[k])
+    return out
+
+
 def cpu_baseline(wl, fraction=0.25, seed=0):
     """The fp64 oracle on this host: kv_write of the whole workload and the prefill of
-    a seeded sample of its query rows (``fraction`` of them), timed once; the rate is
+    a seeded sample of about ``fraction`` of its work -- whole query spans in a seeded
+    order, the last one cut to a leading run of its rows -- timed once; the rate is
     the sample's own algorithmic work over that time."""
     from oracle import workload_oracle as WO
     try:
@@ -278,17 +294,29 @@ def cpu_baseline(wl, fraction=0.25, seed=0):
     except Exception:  # pragma: no cover
         blas = None
     cores = len(os.sched_getaffinity(0))
-    n = wl.q.shape[0]
-    rows = np.sort(np.random.default_rng(seed).choice(n, size=max(1, int(round(fraction * n))), replace=False))
-    work = 4.0 * wl.head_dim * wl.num_q_heads * float(row_pairs(wl)[rows].sum())
+    pairs = row_pairs(wl)
+    budget = fraction * float(pairs.sum())
+    spans = query_span_rows(wl)
+    picked, got = [], 0.0
+    for i in np.random.default_rng(seed).permutation(len(spans)):
+        a, b = spans[i]
+        cum = np.cumsum(pairs[a:b])
+        n = b - a if got + cum[-1] <= budget else int(np.searchsorted(cum, budget - got)) + 1
+        picked.append(np.arange(a, a + n))
+        got += float(cum[n - 1])
+        if got >= budget:
+            break
+    rows = np.sort(np.concatenate(picked))
+    work = 4.0 * wl.head_dim * wl.num_q_heads * float(pairs[rows].sum())
     t0 = time.perf_counter()
     WO.run(wl, rows=rows)
     el = time.perf_counter() - t0
     return {"value": work / el / 1e12, "unit": "TFLOP/s", "cores": int(blas or cores), "kind": "oracle",
             "host_cores": cores,
             "sample": f"{wl.name}: kv_write of all {wl.k_new.shape[0]} fresh rows + prefill of {len(rows)} of its "
-                      f"{n} query tokens (seeded {fraction:.0%} sample) x {wl.num_q_heads} heads, "
-                      f"{work / 1e9:.1f} GFLOP in {el:.2f} s, fp64 NumPy"}
+                      f"{wl.q.shape[0]} query tokens ({len(picked)} query spans in a seeded order, about "
+                      f"{fraction:.0%} of the work) x {wl.num_q_heads} heads, {work / 1e9:.1f} GFLOP in {el:.2f} s, "
+                      f"fp64 NumPy"}
 
 
 def main():
