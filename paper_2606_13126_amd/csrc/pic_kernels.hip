@@ -44,6 +44,75 @@ __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b) {
                                            false);
 }
 
+// ---------------------------------------------------------------------------------
+// K rotation blocks.  A pair (x, y) turns into (x c - y s, x s + y c) as two
+// 2-element dot products with the table entry (c, -s | s, c).  The builtin dot
+// product with a zero addend compiles to a v_mov of zero plus the accumulating
+// VOP2 form; these blocks issue the VOP3P form with an inline-constant zero addend
+// instead.  A DOT result read by another VALU instruction needs 3 wait states on
+// gfx950, which the compiler cannot see inside inline assembly: each block orders
+// its eight dot products before the four conversions that read them, so every
+// result is read at least three instructions after it is written and no s_nop is
+// needed.  Nothing outside a block reads a DOT result of the block.
+// ---------------------------------------------------------------------------------
+
+// Rotate-half (NeoX) pairing, four pairs: A0/B0 hold elements (2m, 2m+1) of the two
+// halves for one m, A1/B1 for the next; e0..e3 are the entries of those four pairs
+// in order (2m, 2m+1, 2m+2, 2m+3).  Outputs replace A*/B* (rounded to bf16, RNE).
+struct Words4 {
+    uint32_t w[4];
+};
+__device__ __forceinline__ Words4 rot4_neox(uint32_t A0, uint32_t B0, uint32_t A1, uint32_t B1, uint2 e0, uint2 e1,
+                                            uint2 e2, uint2 e3) {
+    uint32_t p0, p1, p2, p3;
+    float x0, y0, x1, y1, x2, y2, x3, y3;
+    asm("v_perm_b32 %[p0], %[B0], %[A0], %[slo]\n\t"
+        "v_perm_b32 %[p1], %[B0], %[A0], %[shi]\n\t"
+        "v_perm_b32 %[p2], %[B1], %[A1], %[slo]\n\t"
+        "v_perm_b32 %[p3], %[B1], %[A1], %[shi]\n\t"
+        "v_dot2_f32_bf16 %[x0], %[p0], %[e0x], 0\n\t"
+        "v_dot2_f32_bf16 %[y0], %[p0], %[e0y], 0\n\t"
+        "v_dot2_f32_bf16 %[x1], %[p1], %[e1x], 0\n\t"
+        "v_dot2_f32_bf16 %[y1], %[p1], %[e1y], 0\n\t"
+        "v_dot2_f32_bf16 %[x2], %[p2], %[e2x], 0\n\t"
+        "v_dot2_f32_bf16 %[y2], %[p2], %[e2y], 0\n\t"
+        "v_dot2_f32_bf16 %[x3], %[p3], %[e3x], 0\n\t"
+        "v_dot2_f32_bf16 %[y3], %[p3], %[e3y], 0\n\t"
+        "v_cvt_pk_bf16_f32 %[A0], %[x0], %[x1]\n\t"
+        "v_cvt_pk_bf16_f32 %[B0], %[y0], %[y1]\n\t"
+        "v_cvt_pk_bf16_f32 %[A1], %[x2], %[x3]\n\t"
+        "v_cvt_pk_bf16_f32 %[B1], %[y2], %[y3]"
+        : [A0] "+v"(A0), [B0] "+v"(B0), [A1] "+v"(A1), [B1] "+v"(B1), [p0] "=&v"(p0), [p1] "=&v"(p1),
+          [p2] "=&v"(p2), [p3] "=&v"(p3), [x0] "=&v"(x0), [y0] "=&v"(y0), [x1] "=&v"(x1), [y1] "=&v"(y1),
+          [x2] "=&v"(x2), [y2] "=&v"(y2), [x3] "=&v"(x3), [y3] "=&v"(y3)
+        : [e0x] "v"(e0.x), [e0y] "v"(e0.y), [e1x] "v"(e1.x), [e1y] "v"(e1.y), [e2x] "v"(e2.x), [e2y] "v"(e2.y),
+          [e3x] "v"(e3.x), [e3y] "v"(e3.y), [slo] "s"(0x05040100u), [shi] "s"(0x07060302u));
+    return Words4{{A0, B0, A1, B1}};
+}
+
+// Interleaved (GPT-J) pairing, four pairs: w_i holds the pair (x, y) itself.
+__device__ __forceinline__ Words4 rot4_gptj(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3, uint2 e0, uint2 e1,
+                                            uint2 e2, uint2 e3) {
+    float x0, y0, x1, y1, x2, y2, x3, y3;
+    asm("v_dot2_f32_bf16 %[x0], %[w0], %[e0x], 0\n\t"
+        "v_dot2_f32_bf16 %[y0], %[w0], %[e0y], 0\n\t"
+        "v_dot2_f32_bf16 %[x1], %[w1], %[e1x], 0\n\t"
+        "v_dot2_f32_bf16 %[y1], %[w1], %[e1y], 0\n\t"
+        "v_dot2_f32_bf16 %[x2], %[w2], %[e2x], 0\n\t"
+        "v_dot2_f32_bf16 %[y2], %[w2], %[e2y], 0\n\t"
+        "v_dot2_f32_bf16 %[x3], %[w3], %[e3x], 0\n\t"
+        "v_dot2_f32_bf16 %[y3], %[w3], %[e3y], 0\n\t"
+        "v_cvt_pk_bf16_f32 %[w0], %[x0], %[y0]\n\t"
+        "v_cvt_pk_bf16_f32 %[w1], %[x1], %[y1]\n\t"
+        "v_cvt_pk_bf16_f32 %[w2], %[x2], %[y2]\n\t"
+        "v_cvt_pk_bf16_f32 %[w3], %[x3], %[y3]"
+        : [w0] "+v"(w0), [w1] "+v"(w1), [w2] "+v"(w2), [w3] "+v"(w3), [x0] "=&v"(x0), [y0] "=&v"(y0),
+          [x1] "=&v"(x1), [y1] "=&v"(y1), [x2] "=&v"(x2), [y2] "=&v"(y2), [x3] "=&v"(x3), [y3] "=&v"(y3)
+        : [e0x] "v"(e0.x), [e0y] "v"(e0.y), [e1x] "v"(e1.x), [e1y] "v"(e1.y), [e2x] "v"(e2.x), [e2y] "v"(e2.y),
+          [e3x] "v"(e3.x), [e3y] "v"(e3.y));
+    return Words4{{w0, w1, w2, w3}};
+}
+
 // (a.lo, b.lo) and (a.hi, b.hi) of two bf16 pairs: the rotate-half pairing brings
 // element i of one 8-dim run together with element i of the run half a head
 // further; one byte permute each (bytes 0-3 of the selector pick from a, 4-7 from b)
@@ -632,25 +701,24 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
             }
         }
         if (STYLE == kNeox) {
+            // r.k[0][m] = (x_2m, x_2m+1), r.k[1][m] = (y_2m, y_2m+1)
 #pragma unroll
-            for (int m = 0; m < 4; ++m) {
-                const uint32_t A = r.k[0][m], B = r.k[1][m];
-                const uint32_t p0 = pair_lo(A, B);   // (x_2m, y_2m)
-                const uint32_t p1 = pair_hi(A, B);   // (x_2m+1, y_2m+1)
-                const float x0 = dot2_bf16(p0, e[2 * m].x), y0 = dot2_bf16(p0, e[2 * m].y);
-                const float x1 = dot2_bf16(p1, e[2 * m + 1].x), y1 = dot2_bf16(p1, e[2 * m + 1].y);
-                r.k[0][m] = pack_bf16(x0, x1);
-                r.k[1][m] = pack_bf16(y0, y1);
+            for (int m = 0; m < 4; m += 2) {
+                const Words4 o = rot4_neox(r.k[0][m], r.k[1][m], r.k[0][m + 1], r.k[1][m + 1], e[2 * m], e[2 * m + 1],
+                                           e[2 * m + 2], e[2 * m + 3]);
+                r.k[0][m] = o.w[0];
+                r.k[1][m] = o.w[1];
+                r.k[0][m + 1] = o.w[2];
+                r.k[1][m + 1] = o.w[3];
             }
         } else {
 #pragma unroll
-            for (int h2 = 0; h2 < 2; ++h2)
+            for (int h2 = 0; h2 < 2; ++h2) {
+                const Words4 o = rot4_gptj(r.k[h2][0], r.k[h2][1], r.k[h2][2], r.k[h2][3], e[4 * h2], e[4 * h2 + 1],
+                                           e[4 * h2 + 2], e[4 * h2 + 3]);
 #pragma unroll
-                for (int m = 0; m < 4; ++m) {
-                    const uint32_t xy = r.k[h2][m];
-                    const uint2 ee = e[4 * h2 + m];
-                    r.k[h2][m] = pack_bf16(dot2_bf16(xy, ee.x), dot2_bf16(xy, ee.y));
-                }
+                for (int m = 0; m < 4; ++m) r.k[h2][m] = o.w[m];
+            }
         }
         // a key outside the window (partial tiles only) was loaded as zeros and its
         // entries e are finite (the table's, or the last tile's, or zero), so it is
@@ -729,6 +797,17 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
                     const bf16x8_t af = *reinterpret_cast<const bf16x8_t*>(kb + k_off[kd] + mb * 32 * D);
                     s[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, qb[kd], s[mb], 0, 0, 0);
                 }
+            // keep the K operand reads six reads ahead of their MFMAs (left alone, the
+            // compiler waits on each read right after issuing it)
+#pragma unroll
+            for (int i = 0; i < 6; ++i) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // LDS read
+#pragma unroll
+            for (int i = 0; i < KD * NH - 6; ++i) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                          // MFMA
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            }
+#pragma unroll
+            for (int i = 0; i < 6; ++i) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
             // ---- window mask on tiles that cross a boundary of the visible set: a bit
             // mask of the visible keys relative to this lane's first key of each half
             if (masked) {
@@ -1218,25 +1297,30 @@ __global__ void __launch_bounds__(dec_heads(D) * 64, 1) decode_bf16(const Plan p
 #pragma unroll
             for (int u = 0; u < NTC; ++u) te[u] = *reinterpret_cast<const u32x4_t*>(&sg.tab[t_off[u]]);
             if (STYLE == kNeox) {
+                // te[kd * 4 + m] holds the entries of pairs 2m, 2m+1 of this 8-dim run
 #pragma unroll
                 for (int kd = 0; kd < KD / 2; ++kd)
 #pragma unroll
-                    for (int m = 0; m < 4; ++m) {
-                        const uint32_t A = kf[kd][m], B = kf[kd + KD / 2][m];
-                        const uint32_t p0 = pair_lo(A, B), p1 = pair_hi(A, B);
-                        const u32x4_t e = te[kd * 4 + m];   // pairs 2m, 2m+1 of this 8-dim run
-                        kf[kd][m] = pack_bf16(dot2_bf16(p0, e[0]), dot2_bf16(p1, e[2]));
-                        kf[kd + KD / 2][m] = pack_bf16(dot2_bf16(p0, e[1]), dot2_bf16(p1, e[3]));
+                    for (int m = 0; m < 4; m += 2) {
+                        const u32x4_t ea = te[kd * 4 + m], eb = te[kd * 4 + m + 1];
+                        const Words4 o = rot4_neox(kf[kd][m], kf[kd + KD / 2][m], kf[kd][m + 1], kf[kd + KD / 2][m + 1],
+                                                   make_uint2(ea[0], ea[1]), make_uint2(ea[2], ea[3]),
+                                                   make_uint2(eb[0], eb[1]), make_uint2(eb[2], eb[3]));
+                        kf[kd][m] = o.w[0];
+                        kf[kd + KD / 2][m] = o.w[1];
+                        kf[kd][m + 1] = o.w[2];
+                        kf[kd + KD / 2][m + 1] = o.w[3];
                     }
             } else {
 #pragma unroll
-                for (int kd = 0; kd < KD; ++kd)
+                for (int kd = 0; kd < KD; ++kd) {
+                    const u32x4_t ea = te[kd * 2], eb = te[kd * 2 + 1];
+                    const Words4 o = rot4_gptj(kf[kd][0], kf[kd][1], kf[kd][2], kf[kd][3], make_uint2(ea[0], ea[1]),
+                                               make_uint2(ea[2], ea[3]), make_uint2(eb[0], eb[1]),
+                                               make_uint2(eb[2], eb[3]));
 #pragma unroll
-                    for (int m = 0; m < 4; ++m) {
-                        const u32x4_t e = te[kd * 2 + m / 2];
-                        const uint32_t ex = e[2 * (m & 1)], ey = e[2 * (m & 1) + 1];
-                        kf[kd][m] = pack_bf16(dot2_bf16(kf[kd][m], ex), dot2_bf16(kf[kd][m], ey));
-                    }
+                    for (int m = 0; m < 4; ++m) kf[kd][m] = o.w[m];
+                }
             }
         }
         f32x4_t sc4 = f32x4_t{0.f, 0.f, 0.f, 0.f};
