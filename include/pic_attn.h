@@ -113,16 +113,17 @@ typedef struct pic_batch_dev {
     const int32_t* positions;    /* DEVICE [sum L_r], any int32 values */
 } pic_batch_dev;
 
-/* Optional cos/sin table (the paper's cos_sin lookup, Sec. 3.2.2): one 8-byte entry
- * per (position p in [0, len), pair i in [0, D/2)), from cos/sin(p*omega_i) computed
- * in float64 (omega_i = 0 for pairs past rotary_dim).  A table belongs to the
- * frequencies of the cfg that built it.  PIC_F32 tables hold (cos, sin) as two float32; PIC_BF16 tables hold
- * (cos, -sin, sin, cos) as four bf16, so that the kernel rotates a pair (x, y) with
- * two 2-element dot products.  Built by pic_rope_table_build for cfg->dtype.
+/* Optional cos/sin table (the paper's cos_sin lookup, Sec. 3.2.2): one entry per
+ * (position p in [0, len), pair i in [0, D/2)), from cos/sin(p*omega_i) computed in
+ * float64 (omega_i = 0 for pairs past rotary_dim).  A table belongs to the
+ * frequencies of the cfg that built it.  PIC_F32 tables hold (cos, sin) as two
+ * float32 (8 bytes per entry); PIC_BF16 tables hold (cos, sin) as a bf16 pair (4
+ * bytes), with which the kernel rotates a pair (x, y) by two 2-element dot products.
+ * Built by pic_rope_table_build for cfg->dtype; pic_rope_table_bytes gives the size.
  * Positions outside [0, len), and every position when data is NULL, are rotated
  * with cos/sin computed in the kernel from an exact fixed-point phase. */
 typedef struct pic_rope_table {
-    const void* data; /* DEVICE [len][D/2] 8-byte entries, or NULL */
+    const void* data; /* DEVICE [len][D/2] entries (8 bytes for PIC_F32, 4 for PIC_BF16), or NULL */
     int32_t len;
 } pic_rope_table;
 

@@ -171,7 +171,9 @@ def pic_rope_table_bytes(cfg: pic_config, num_positions: int) -> int:
 
 
 def pic_rope_table_build(cfg: pic_config, table, stream=None) -> None:
-    """table: float32 tensor [num_positions][D/2][2] on the device."""
+    """table: device tensor of pic_rope_table_bytes(cfg, num_positions) bytes whose first
+    dimension is num_positions ([n][D/2][2] float32 for PIC_F32, [n][D/2] 4-byte words
+    for PIC_BF16)."""
     _check(_lib.pic_rope_table_build(ctypes.byref(cfg), int(table.shape[0]), _ptr(table), _stream(stream)))
 
 

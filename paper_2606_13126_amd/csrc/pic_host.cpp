@@ -450,7 +450,8 @@ pic_status pic_rope_table_bytes(const pic_config* cfg, int32_t num_positions, si
     pic_status st = check_config(cfg);
     if (st) return st;
     if (num_positions < 0 || bytes == nullptr) return fail(PIC_EINVAL, "bad num_positions or bytes pointer");
-    *bytes = (size_t)num_positions * (cfg->head_dim / 2) * 2 * sizeof(float);
+    // float32 tables hold (cos, sin) as two floats, bf16 tables as one bf16 pair
+    *bytes = (size_t)num_positions * (cfg->head_dim / 2) * (cfg->dtype == PIC_F32 ? 8 : 4);
     return PIC_OK;
 }
 

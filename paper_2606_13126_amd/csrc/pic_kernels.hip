@@ -45,71 +45,81 @@ __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b) {
 }
 
 // ---------------------------------------------------------------------------------
-// K rotation blocks.  A pair (x, y) turns into (x c - y s, x s + y c) as two
-// 2-element dot products with the table entry (c, -s | s, c).  The builtin dot
-// product with a zero addend compiles to a v_mov of zero plus the accumulating
-// VOP2 form; these blocks issue the VOP3P form with an inline-constant zero addend
-// instead.  A DOT result read by another VALU instruction needs 3 wait states on
-// gfx950, which the compiler cannot see inside inline assembly: each block orders
-// its eight dot products before the four conversions that read them, so every
-// result is read at least three instructions after it is written and no s_nop is
-// needed.  Nothing outside a block reads a DOT result of the block.
+// K rotation blocks.  A pair (x, y) turns into (x c - y s, y c + x s) as two
+// 2-element dot products with the table entry e = (c, s): (x, y).(c, -s), the sign
+// applied by the instruction's neg_hi modifier, and (y, x).(c, s).  The builtin
+// dot product with a zero addend compiles to a v_mov of zero plus the accumulating
+// VOP2 form (which has no modifiers); these blocks issue the VOP3P form with an
+// inline-constant zero addend.  A DOT result read by another VALU instruction needs
+// 3 wait states on gfx950, which the compiler cannot see inside inline assembly:
+// each block orders its eight dot products before the four conversions that read
+// them, so every result is read at least three instructions after it is written and
+// no s_nop is needed.  Nothing outside a block reads a DOT result of the block.
 // ---------------------------------------------------------------------------------
-
-// Rotate-half (NeoX) pairing, four pairs: A0/B0 hold elements (2m, 2m+1) of the two
-// halves for one m, A1/B1 for the next; e0..e3 are the entries of those four pairs
-// in order (2m, 2m+1, 2m+2, 2m+3).  Outputs replace A*/B* (rounded to bf16, RNE).
 struct Words4 {
     uint32_t w[4];
 };
-__device__ __forceinline__ Words4 rot4_neox(uint32_t A0, uint32_t B0, uint32_t A1, uint32_t B1, uint2 e0, uint2 e1,
-                                            uint2 e2, uint2 e3) {
-    uint32_t p0, p1, p2, p3;
+
+// Rotate-half (NeoX) pairing, four pairs: A0/B0 hold elements (2m, 2m+1) of the two
+// halves for one m, A1/B1 for the next; e0..e3 are the entries of those four pairs
+// in order.  Returns the rotated A0, B0, A1, B1 (rounded to bf16, RNE).
+__device__ __forceinline__ Words4 rot4_neox(uint32_t A0, uint32_t B0, uint32_t A1, uint32_t B1, uint32_t e0,
+                                            uint32_t e1, uint32_t e2, uint32_t e3) {
+    uint32_t p0, p1, p2, p3, q0, q1, q2, q3;
     float x0, y0, x1, y1, x2, y2, x3, y3;
-    asm("v_perm_b32 %[p0], %[B0], %[A0], %[slo]\n\t"
+    asm("v_perm_b32 %[p0], %[B0], %[A0], %[slo]\n\t"   // (x_2m, y_2m)
+        "v_perm_b32 %[q0], %[A0], %[B0], %[slo]\n\t"   // (y_2m, x_2m)
         "v_perm_b32 %[p1], %[B0], %[A0], %[shi]\n\t"
+        "v_perm_b32 %[q1], %[A0], %[B0], %[shi]\n\t"
         "v_perm_b32 %[p2], %[B1], %[A1], %[slo]\n\t"
+        "v_perm_b32 %[q2], %[A1], %[B1], %[slo]\n\t"
         "v_perm_b32 %[p3], %[B1], %[A1], %[shi]\n\t"
-        "v_dot2_f32_bf16 %[x0], %[p0], %[e0x], 0\n\t"
-        "v_dot2_f32_bf16 %[y0], %[p0], %[e0y], 0\n\t"
-        "v_dot2_f32_bf16 %[x1], %[p1], %[e1x], 0\n\t"
-        "v_dot2_f32_bf16 %[y1], %[p1], %[e1y], 0\n\t"
-        "v_dot2_f32_bf16 %[x2], %[p2], %[e2x], 0\n\t"
-        "v_dot2_f32_bf16 %[y2], %[p2], %[e2y], 0\n\t"
-        "v_dot2_f32_bf16 %[x3], %[p3], %[e3x], 0\n\t"
-        "v_dot2_f32_bf16 %[y3], %[p3], %[e3y], 0\n\t"
+        "v_perm_b32 %[q3], %[A1], %[B1], %[shi]\n\t"
+        "v_dot2_f32_bf16 %[x0], %[p0], %[e0], 0 neg_hi:[0,1,0]\n\t"
+        "v_dot2_f32_bf16 %[y0], %[q0], %[e0], 0\n\t"
+        "v_dot2_f32_bf16 %[x1], %[p1], %[e1], 0 neg_hi:[0,1,0]\n\t"
+        "v_dot2_f32_bf16 %[y1], %[q1], %[e1], 0\n\t"
+        "v_dot2_f32_bf16 %[x2], %[p2], %[e2], 0 neg_hi:[0,1,0]\n\t"
+        "v_dot2_f32_bf16 %[y2], %[q2], %[e2], 0\n\t"
+        "v_dot2_f32_bf16 %[x3], %[p3], %[e3], 0 neg_hi:[0,1,0]\n\t"
+        "v_dot2_f32_bf16 %[y3], %[q3], %[e3], 0\n\t"
         "v_cvt_pk_bf16_f32 %[A0], %[x0], %[x1]\n\t"
         "v_cvt_pk_bf16_f32 %[B0], %[y0], %[y1]\n\t"
         "v_cvt_pk_bf16_f32 %[A1], %[x2], %[x3]\n\t"
         "v_cvt_pk_bf16_f32 %[B1], %[y2], %[y3]"
         : [A0] "+v"(A0), [B0] "+v"(B0), [A1] "+v"(A1), [B1] "+v"(B1), [p0] "=&v"(p0), [p1] "=&v"(p1),
-          [p2] "=&v"(p2), [p3] "=&v"(p3), [x0] "=&v"(x0), [y0] "=&v"(y0), [x1] "=&v"(x1), [y1] "=&v"(y1),
-          [x2] "=&v"(x2), [y2] "=&v"(y2), [x3] "=&v"(x3), [y3] "=&v"(y3)
-        : [e0x] "v"(e0.x), [e0y] "v"(e0.y), [e1x] "v"(e1.x), [e1y] "v"(e1.y), [e2x] "v"(e2.x), [e2y] "v"(e2.y),
-          [e3x] "v"(e3.x), [e3y] "v"(e3.y), [slo] "s"(0x05040100u), [shi] "s"(0x07060302u));
+          [p2] "=&v"(p2), [p3] "=&v"(p3), [q0] "=&v"(q0), [q1] "=&v"(q1), [q2] "=&v"(q2), [q3] "=&v"(q3),
+          [x0] "=&v"(x0), [y0] "=&v"(y0), [x1] "=&v"(x1), [y1] "=&v"(y1), [x2] "=&v"(x2), [y2] "=&v"(y2),
+          [x3] "=&v"(x3), [y3] "=&v"(y3)
+        : [e0] "v"(e0), [e1] "v"(e1), [e2] "v"(e2), [e3] "v"(e3), [slo] "s"(0x05040100u), [shi] "s"(0x07060302u));
     return Words4{{A0, B0, A1, B1}};
 }
 
 // Interleaved (GPT-J) pairing, four pairs: w_i holds the pair (x, y) itself.
-__device__ __forceinline__ Words4 rot4_gptj(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3, uint2 e0, uint2 e1,
-                                            uint2 e2, uint2 e3) {
+__device__ __forceinline__ Words4 rot4_gptj(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3, uint32_t e0,
+                                            uint32_t e1, uint32_t e2, uint32_t e3) {
+    uint32_t q0, q1, q2, q3;
     float x0, y0, x1, y1, x2, y2, x3, y3;
-    asm("v_dot2_f32_bf16 %[x0], %[w0], %[e0x], 0\n\t"
-        "v_dot2_f32_bf16 %[y0], %[w0], %[e0y], 0\n\t"
-        "v_dot2_f32_bf16 %[x1], %[w1], %[e1x], 0\n\t"
-        "v_dot2_f32_bf16 %[y1], %[w1], %[e1y], 0\n\t"
-        "v_dot2_f32_bf16 %[x2], %[w2], %[e2x], 0\n\t"
-        "v_dot2_f32_bf16 %[y2], %[w2], %[e2y], 0\n\t"
-        "v_dot2_f32_bf16 %[x3], %[w3], %[e3x], 0\n\t"
-        "v_dot2_f32_bf16 %[y3], %[w3], %[e3y], 0\n\t"
+    asm("v_alignbit_b32 %[q0], %[w0], %[w0], 16\n\t"   // (y, x)
+        "v_alignbit_b32 %[q1], %[w1], %[w1], 16\n\t"
+        "v_alignbit_b32 %[q2], %[w2], %[w2], 16\n\t"
+        "v_alignbit_b32 %[q3], %[w3], %[w3], 16\n\t"
+        "v_dot2_f32_bf16 %[x0], %[w0], %[e0], 0 neg_hi:[0,1,0]\n\t"
+        "v_dot2_f32_bf16 %[y0], %[q0], %[e0], 0\n\t"
+        "v_dot2_f32_bf16 %[x1], %[w1], %[e1], 0 neg_hi:[0,1,0]\n\t"
+        "v_dot2_f32_bf16 %[y1], %[q1], %[e1], 0\n\t"
+        "v_dot2_f32_bf16 %[x2], %[w2], %[e2], 0 neg_hi:[0,1,0]\n\t"
+        "v_dot2_f32_bf16 %[y2], %[q2], %[e2], 0\n\t"
+        "v_dot2_f32_bf16 %[x3], %[w3], %[e3], 0 neg_hi:[0,1,0]\n\t"
+        "v_dot2_f32_bf16 %[y3], %[q3], %[e3], 0\n\t"
         "v_cvt_pk_bf16_f32 %[w0], %[x0], %[y0]\n\t"
         "v_cvt_pk_bf16_f32 %[w1], %[x1], %[y1]\n\t"
         "v_cvt_pk_bf16_f32 %[w2], %[x2], %[y2]\n\t"
         "v_cvt_pk_bf16_f32 %[w3], %[x3], %[y3]"
-        : [w0] "+v"(w0), [w1] "+v"(w1), [w2] "+v"(w2), [w3] "+v"(w3), [x0] "=&v"(x0), [y0] "=&v"(y0),
-          [x1] "=&v"(x1), [y1] "=&v"(y1), [x2] "=&v"(x2), [y2] "=&v"(y2), [x3] "=&v"(x3), [y3] "=&v"(y3)
-        : [e0x] "v"(e0.x), [e0y] "v"(e0.y), [e1x] "v"(e1.x), [e1y] "v"(e1.y), [e2x] "v"(e2.x), [e2y] "v"(e2.y),
-          [e3x] "v"(e3.x), [e3y] "v"(e3.y));
+        : [w0] "+v"(w0), [w1] "+v"(w1), [w2] "+v"(w2), [w3] "+v"(w3), [q0] "=&v"(q0), [q1] "=&v"(q1),
+          [q2] "=&v"(q2), [q3] "=&v"(q3), [x0] "=&v"(x0), [y0] "=&v"(y0), [x1] "=&v"(x1), [y1] "=&v"(y1),
+          [x2] "=&v"(x2), [y2] "=&v"(y2), [x3] "=&v"(x3), [y3] "=&v"(y3)
+        : [e0] "v"(e0), [e1] "v"(e1), [e2] "v"(e2), [e3] "v"(e3));
     return Words4{{w0, w1, w2, w3}};
 }
 
@@ -156,26 +166,26 @@ __device__ __forceinline__ void rope_cs_f64(int32_t pos, uint64_t step, double& 
 __device__ __forceinline__ int model_chunk(uint64_t map, int c) { return (int)((map >> (4 * c)) & 15); }
 
 // Table entries: float32 kernels read (cos, sin) as two floats; bf16 kernels read
-// (cos, -sin) and (sin, cos) as two bf16 pairs, so that rotating a pair (x, y) is
-// two 2-element dot products: x' = (x, y).(c, -s), y' = (x, y).(s, c).
-__device__ __forceinline__ void cs_from_bf16_entry(uint2 w, float& c, float& s) {
-    c = bf_lo(w.x);
-    s = bf_lo(w.y);
-}
-__device__ __forceinline__ uint2 bf16_entry(float c, float s) { return make_uint2(pack_bf16(c, -s), pack_bf16(s, c)); }
+// (cos, sin) as one bf16 pair, so that rotating a pair (x, y) is two 2-element dot
+// products: x' = (x, y).(c, -s) with the sign folded into the instruction, and
+// y' = (y, x).(c, s).
+__device__ __forceinline__ uint32_t bf16_entry(float c, float s) { return pack_bf16(c, s); }
 
-// cos/sin of N consecutive frequencies i0 .. i0+N-1 at position pos from a bf16
-// table when pos is inside it, else computed.
+// cos/sin of N consecutive frequencies i0 .. i0+N-1 (i0 a multiple of 4) at
+// position pos from a bf16 table when pos is inside it, else computed.
 template <int N, bool TABLE>
 __device__ __forceinline__ void rope_cs_n(const float* __restrict__ table, int rope_len, int half,
                                           const uint64_t* fstep, int32_t pos, int i0, float* c, float* s) {
     if (TABLE && (uint32_t)pos < (uint32_t)rope_len) {
-        const uint4* t = reinterpret_cast<const uint4*>(table + ((size_t)pos * half + i0) * 2);
+        const u32x4_t* t = reinterpret_cast<const u32x4_t*>(reinterpret_cast<const uint32_t*>(table) + (size_t)pos * half + i0);
 #pragma unroll
-        for (int k = 0; k < N / 2; ++k) {
-            const uint4 v = t[k];
-            cs_from_bf16_entry(make_uint2(v.x, v.y), c[2 * k], s[2 * k]);
-            cs_from_bf16_entry(make_uint2(v.z, v.w), c[2 * k + 1], s[2 * k + 1]);
+        for (int k = 0; k < N / 4; ++k) {
+            const u32x4_t v = t[k];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                c[4 * k + j] = bf_lo(v[j]);
+                s[4 * k + j] = bf_hi(v[j]);
+            }
         }
     } else {
 #pragma unroll
@@ -266,17 +276,19 @@ __global__ void __launch_bounds__(256) blocks_copy_kernel(u32x4_t* __restrict__ 
 
 // ---------------------------------------------------------------------------------
 // rope_table: entry [p][i] from cos/sin(p * omega_i) in float64, stored as float32
-// (cos, sin) or as bf16 (cos, -sin, sin, cos).
+// (cos, sin) or as a bf16 pair (cos, sin).
 // ---------------------------------------------------------------------------------
-__global__ void __launch_bounds__(256) rope_table_kernel(uint2* __restrict__ table, int n_pos, int half,
+__global__ void __launch_bounds__(256) rope_table_kernel(void* __restrict__ table, int n_pos, int half,
                                                          RopeSteps steps, bool bf16_pairs) {
     const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (idx >= (int64_t)n_pos * half) return;
     const int p = (int)(idx / half), i = (int)(idx - (int64_t)p * half);
     double c, s;
     rope_cs_f64(p, steps.s[i], c, s);
-    table[idx] = bf16_pairs ? bf16_entry((float)c, (float)s)
-                            : make_uint2(__float_as_uint((float)c), __float_as_uint((float)s));
+    if (bf16_pairs)
+        static_cast<uint32_t*>(table)[idx] = bf16_entry((float)c, (float)s);
+    else
+        static_cast<uint2*>(table)[idx] = make_uint2(__float_as_uint((float)c), __float_as_uint((float)s));
 }
 
 // ---------------------------------------------------------------------------------
@@ -286,7 +298,7 @@ template <typename T, int STYLE>
 __global__ void __launch_bounds__(256) rope_rotate_kernel(T* __restrict__ x, int64_t n_pairs, int heads, int d,
                                                           int rot_half, RopeSteps steps,
                                                           const int32_t* __restrict__ positions,
-                                                          const uint2* __restrict__ table, int rope_len) {
+                                                          const void* __restrict__ table, int rope_len) {
     const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (idx >= n_pairs) return;
     const int half = d / 2;
@@ -296,12 +308,14 @@ __global__ void __launch_bounds__(256) rope_rotate_kernel(T* __restrict__ x, int
     const int32_t pos = positions[rh / heads];
     float c, s;
     if (table != nullptr && (uint32_t)pos < (uint32_t)rope_len) {
-        const uint2 v = table[(size_t)pos * half + i];
         if (sizeof(T) == 4) {
+            const uint2 v = static_cast<const uint2*>(table)[(size_t)pos * half + i];
             c = __uint_as_float(v.x);
             s = __uint_as_float(v.y);
         } else {
-            cs_from_bf16_entry(v, c, s);
+            const uint32_t v = static_cast<const uint32_t*>(table)[(size_t)pos * half + i];
+            c = bf_lo(v);
+            s = bf_hi(v);
         }
     } else {
         rope_cs(pos, steps.s[i], c, s);
@@ -391,10 +405,10 @@ __device__ __forceinline__ s16x4_t lds_read_tr(lds_u16_t* p) {
 
 // One thread's share of a K tile in flight when K is rotated on its way to LDS:
 // 16 elements of one key (NeoX: 8 from each half; GPT-J: 16 consecutive) and the
-// table entries of their 8 pairs.
+// bf16 (cos, sin) entries of their 8 pairs.
 struct TileRegs {
     u32x4_t k[2];
-    float4 cs[4];
+    u32x4_t cs[2];
     int32_t pos;
     bool ok;
 };
@@ -667,9 +681,10 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
                 r.k[1] = *reinterpret_cast<const u32x4_t*>(kp + sc * 16 + 8);
             }
             if (TABLE && (uint32_t)r.pos < (uint32_t)a.rope_len) {
-                const float4* tp = reinterpret_cast<const float4*>(a.rope_table + ((size_t)r.pos * HALF + sc * 8) * 2);
-#pragma unroll
-                for (int k = 0; k < 4; ++k) r.cs[k] = tp[k];
+                const u32x4_t* tp = reinterpret_cast<const u32x4_t*>(reinterpret_cast<const uint32_t*>(a.rope_table) +
+                                                                     (size_t)r.pos * HALF + sc * 8);
+                r.cs[0] = tp[0];
+                r.cs[1] = tp[1];
             }
         }
         }
@@ -680,15 +695,12 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
         for (int u = 0; u < SU; ++u) {
         TileRegs& r = rr[u];
         const int kr = kk + u * KSTEP;
-        // e[k] = (cos, -sin | sin, cos) of pair sc*8 + k as bf16: from the table, or
-        // computed for keys whose position lies outside it (a wave-uniform branch, so
-        // the common all-in-table case runs no fallback code)
-        uint2 e[8];
+        // e[k] = (cos, sin) of pair sc*8 + k as bf16: from the table, or computed for
+        // keys whose position lies outside it (a wave-uniform branch, so the common
+        // all-in-table case runs no fallback code)
+        uint32_t e[8];
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            e[2 * k] = make_uint2(__float_as_uint(r.cs[k].x), __float_as_uint(r.cs[k].y));
-            e[2 * k + 1] = make_uint2(__float_as_uint(r.cs[k].z), __float_as_uint(r.cs[k].w));
-        }
+        for (int k = 0; k < 8; ++k) e[k] = r.cs[k / 4][k % 4];
         const bool need_cs = r.ok && !(TABLE && (uint32_t)r.pos < (uint32_t)a.rope_len);
         if (!TABLE || __builtin_amdgcn_ballot_w64(need_cs) != 0) {
             if (need_cs) {
@@ -1016,9 +1028,9 @@ template <int D>
 constexpr int dec_stages() {
     // K + V of the workgroup's heads x 16 keys, plus the tile's cos/sin rows, per
     // stage, within 144 KB of LDS
-    return 147456 / (2 * dec_heads(D) * kDecKeys * D * 2 + kDecKeys * D / 2 * 8) > 4
+    return 147456 / (2 * dec_heads(D) * kDecKeys * D * 2 + kDecKeys * D / 2 * 4) > 4
                ? 4
-               : 147456 / (2 * dec_heads(D) * kDecKeys * D * 2 + kDecKeys * D / 2 * 8);
+               : 147456 / (2 * dec_heads(D) * kDecKeys * D * 2 + kDecKeys * D / 2 * 4);
 }
 
 // One pipeline stage of the decode kernel in LDS.  Each stage is its own LDS
@@ -1028,7 +1040,7 @@ template <int D, bool ROPE>
 struct DecStage {
     uint16_t k[dec_heads(D) * kDecKeys * D];   // [head][key][D], chunks swizzled by key
     uint16_t v[dec_heads(D) * kDecKeys * D];
-    uint2 tab[ROPE ? kDecKeys * D / 2 : 2];     // [key][pair] (c,-s | s,c), chunks swizzled by key
+    uint32_t tab[ROPE ? kDecKeys * D / 2 : 4];  // [key][pair] bf16 (c, s), 16-byte chunks swizzled by key
 };
 
 template <int I>
@@ -1067,11 +1079,11 @@ __global__ void __launch_bounds__(dec_heads(D) * 64, 1) decode_bf16(const Plan p
     constexpr int NT = HW * 64;            // threads
     constexpr int HSZ = TK * D;            // elements of one head's tile
     constexpr int DPL = HW * HSZ / 8 / NT; // 16-byte direct loads per lane per tile, each of K and V
-    constexpr int TCH = TK * HALF / 2;     // 16-byte chunks (2 entries) of the tile's cos/sin rows
-    constexpr int TROW = HALF / 2;         // chunks per cos/sin row
+    constexpr int TROW = HALF / 4;         // 16-byte chunks (4 entries) per cos/sin row
+    constexpr int TCH = TK * TROW;         // chunks of the tile's cos/sin rows
     constexpr int NST = dec_stages<D>();   // pipeline stages (tiles resident in LDS)
     constexpr int LPS = 2 * DPL;           // unconditional loads per lane per stage
-    static_assert(DPL >= 1 && TROW >= 16 && NST >= 2 && NST <= 4, "decode tile shape");
+    static_assert(DPL >= 1 && TROW >= 8 && NST >= 2 && NST <= 4, "decode tile shape");
     static_assert((NST - 2) * LPS < 64, "vmcnt range");
     typedef DecStage<D, ROPE> Stage;
 
@@ -1199,8 +1211,8 @@ __global__ void __launch_bounds__(dec_heads(D) * 64, 1) decode_bf16(const Plan p
     // wave `wave` fills 16-byte chunk p = (i*HW + wave)*64 + lane of the stage's K
     // and V: head p / (HSZ/8), key row, physical chunk pc holding logical chunk
     // pc ^ swz(key).  Chunk c < TCH of the tile's cos/sin rows (key c / TROW,
-    // physical chunk pc holding logical chunk pc ^ key: conflict-free reads across
-    // 16 keys) comes from the table, or is computed for positions outside it.  The
+    // physical chunk pc holding logical chunk pc ^ (key % TROW): conflict-free reads
+    // across the keys) comes from the table, or is computed for positions outside it.  The
     // positions of tile u + NST - 1 (the next tile issued after this one) go out
     // first, into the slot tile u - 1 has finished with.
     auto issue_tile = [&](auto b, int u) {
@@ -1214,18 +1226,22 @@ __global__ void __launch_bounds__(dec_heads(D) * 64, 1) decode_bf16(const Plan p
             for (int k = 0; k * NT < TCH; ++k) {
                 const int c = k * NT + tid;
                 if (c < TCH) {
-                    const int tkey = c / TROW, lc = (c % TROW) ^ tkey;
+                    const int tkey = c / TROW, lc = (c % TROW) ^ (tkey & (TROW - 1));
                     const int32_t pos = pp[tkey];
                     const bool in_table = TABLE && (uint32_t)pos < (uint32_t)a.rope_len;
                     if (in_table)
-                        dma_lds16(a.rope_table + ((size_t)pos * HALF + 2 * lc) * 2, &sg.tab[(k * NT + wave * 64) * 2]);
+                        dma_lds16(reinterpret_cast<const uint32_t*>(a.rope_table) + (size_t)pos * HALF + 4 * lc,
+                                  &sg.tab[(k * NT + wave * 64) * 4]);
                     if (!TABLE || __builtin_amdgcn_ballot_w64(!in_table) != 0) {
                         if (!in_table) {
-                            float c0, s0, c1, s1;
-                            rope_cs(pos, fstep[2 * lc], c0, s0);
-                            rope_cs(pos, fstep[2 * lc + 1], c1, s1);
-                            const uint2 e0 = bf16_entry(c0, s0), e1 = bf16_entry(c1, s1);
-                            *reinterpret_cast<u32x4_t*>(&sg.tab[c * 2]) = u32x4_t{e0.x, e0.y, e1.x, e1.y};
+                            u32x4_t w;
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) {
+                                float ce, se;
+                                rope_cs(pos, fstep[4 * lc + e], ce, se);
+                                w[e] = bf16_entry(ce, se);
+                            }
+                            *reinterpret_cast<u32x4_t*>(&sg.tab[c * 4]) = w;
                         }
                     }
                 }
@@ -1252,19 +1268,19 @@ __global__ void __launch_bounds__(dec_heads(D) * 64, 1) decode_bf16(const Plan p
 
     // per-lane LDS offsets within one head's tile: K operand rows (key c16, logical
     // chunk 4*kd + q4), the cos/sin chunks of the pairs those dims belong to (NeoX:
-    // pairs 32*kd + 8*q4 + e, kd < KD/2, 4 chunks each; GPT-J: pairs 16*kd + 4*q4 + e,
-    // 2 chunks each), and the transposing V reads (key 4*q4 + (lane%16)/4, dims
+    // pairs 32*kd + 8*q4 + e, kd < KD/2, 2 chunks each; GPT-J: pairs 16*kd + 4*q4 + e,
+    // 1 chunk each), and the transposing V reads (key 4*q4 + (lane%16)/4, dims
     // 16*db + 4*(lane%4))
     int k_off[KD];
 #pragma unroll
     for (int kd = 0; kd < KD; ++kd)
         k_off[kd] = wave * HSZ + c16 * D + ((model_chunk(a.chunk_map, kd * 4 + q4) ^ swz<D>(c16)) << 3);
-    constexpr int NTC = STYLE == kNeox ? 4 * (KD / 2) : 2 * KD;
+    constexpr int NTC = KD;   // NeoX: 2 chunks for each of the KD/2 steps; GPT-J: 1 for each of KD
     int t_off[NTC];
 #pragma unroll
     for (int u = 0; u < NTC; ++u) {
-        const int lc = STYLE == kNeox ? (u / 4) * 16 + 4 * q4 + (u % 4) : (u / 2) * 8 + 2 * q4 + (u % 2);
-        t_off[u] = c16 * HALF + 2 * (lc ^ c16);
+        const int lc = STYLE == kNeox ? (u / 2) * 8 + 2 * q4 + (u % 2) : u * 4 + q4;
+        t_off[u] = c16 * HALF + 4 * (lc ^ (c16 & (TROW - 1)));
     }
     int v_off[DB];
     {
@@ -1292,20 +1308,20 @@ __global__ void __launch_bounds__(dec_heads(D) * 64, 1) decode_bf16(const Plan p
 #pragma unroll
         for (int kd = 0; kd < KD; ++kd) kf[kd] = *reinterpret_cast<const u32x4_t*>(sg.k + k_off[kd]);
         if (ROPE) {
-            // rotate the K operand in registers with entries (c,-s | s,c)
+            // rotate the K operand in registers with bf16 entries (c, s)
             u32x4_t te[NTC];
 #pragma unroll
             for (int u = 0; u < NTC; ++u) te[u] = *reinterpret_cast<const u32x4_t*>(&sg.tab[t_off[u]]);
             if (STYLE == kNeox) {
-                // te[kd * 4 + m] holds the entries of pairs 2m, 2m+1 of this 8-dim run
+                // te[2 kd] and te[2 kd + 1] hold the entries of pairs 0-3 and 4-7 of this
+                // lane's 8-pair run; kf[kd][m] = (x_2m, x_2m+1), kf[kd + KD/2][m] = (y_2m, y_2m+1)
 #pragma unroll
                 for (int kd = 0; kd < KD / 2; ++kd)
 #pragma unroll
                     for (int m = 0; m < 4; m += 2) {
-                        const u32x4_t ea = te[kd * 4 + m], eb = te[kd * 4 + m + 1];
+                        const u32x4_t ee = te[2 * kd + m / 2];
                         const Words4 o = rot4_neox(kf[kd][m], kf[kd + KD / 2][m], kf[kd][m + 1], kf[kd + KD / 2][m + 1],
-                                                   make_uint2(ea[0], ea[1]), make_uint2(ea[2], ea[3]),
-                                                   make_uint2(eb[0], eb[1]), make_uint2(eb[2], eb[3]));
+                                                   ee[0], ee[1], ee[2], ee[3]);
                         kf[kd][m] = o.w[0];
                         kf[kd + KD / 2][m] = o.w[1];
                         kf[kd][m + 1] = o.w[2];
@@ -1314,10 +1330,8 @@ __global__ void __launch_bounds__(dec_heads(D) * 64, 1) decode_bf16(const Plan p
             } else {
 #pragma unroll
                 for (int kd = 0; kd < KD; ++kd) {
-                    const u32x4_t ea = te[kd * 2], eb = te[kd * 2 + 1];
-                    const Words4 o = rot4_gptj(kf[kd][0], kf[kd][1], kf[kd][2], kf[kd][3], make_uint2(ea[0], ea[1]),
-                                               make_uint2(ea[2], ea[3]), make_uint2(eb[0], eb[1]),
-                                               make_uint2(eb[2], eb[3]));
+                    const u32x4_t ee = te[kd];
+                    const Words4 o = rot4_gptj(kf[kd][0], kf[kd][1], kf[kd][2], kf[kd][3], ee[0], ee[1], ee[2], ee[3]);
 #pragma unroll
                     for (int m = 0; m < 4; ++m) kf[kd][m] = o.w[m];
                 }
@@ -1647,7 +1661,7 @@ int launch_rope_table(int dtype, int d, const RopeSteps& steps, int n_pos, float
     const int64_t n = (int64_t)n_pos * (d / 2);
     if (n == 0) return hipSuccess;
     hipLaunchKernelGGL(rope_table_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, (hipStream_t)stream,
-                       reinterpret_cast<uint2*>(table), n_pos, d / 2, steps, dtype != 1);
+                       static_cast<void*>(table), n_pos, d / 2, steps, dtype != 1);
     return hipGetLastError();
 }
 
@@ -1656,7 +1670,7 @@ int launch_rope_rotate(int dtype, int style, int d, int rot_half, const RopeStep
     const int64_t n_pairs = (int64_t)n * heads * (d / 2);
     if (n_pairs == 0) return hipSuccess;
     const dim3 grid((unsigned)((n_pairs + 255) / 256));
-    const uint2* t = reinterpret_cast<const uint2*>(table);
+    const void* t = table;
     hipStream_t st = (hipStream_t)stream;
     if (dtype == 1) {
         if (style == kNeox)

@@ -43,7 +43,10 @@ class DeviceBatch:
         self.table = None
         if table_positions:
             half = wl.head_dim // 2
-            self.table = torch.empty((table_positions, half, 2), dtype=torch.float32, device=device)
+            # float32 entries are (cos, sin) float pairs, bf16 entries one bf16 pair
+            shape = (table_positions, half, 2) if wl.dtype == torch.float32 else (table_positions, half)
+            self.table = torch.empty(shape, dtype=torch.float32, device=device)
+            assert self.table.numel() * 4 == B.pic_rope_table_bytes(self.cfg, table_positions)
             B.pic_rope_table_build(self.cfg, self.table)
 
     def write(self, stream=None):
