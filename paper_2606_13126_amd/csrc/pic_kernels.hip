@@ -391,6 +391,16 @@ __device__ __forceinline__ int swz(int key) {
     return (key >> 1) & 7;
 }
 
+// The decode kernel's 16-key tiles: D = 128 puts key bits 0-1 on chunk bits 2-3,
+// key bit 2 on chunk bit 1 and key bit 3 on chunk bit 0.  The 16 keys still get 16
+// different patterns (conflict-free K operand reads), and the transposing V reads
+// of 8 consecutive keys x 2 chunk halves (a 32-lane pass) cover all 16 chunks once.
+template <int D>
+__device__ __forceinline__ int dswz(int key) {
+    if (D == 128) return ((key & 3) << 2) | (((key >> 2) & 1) << 1) | ((key >> 3) & 1);
+    return swz<D>(key);
+}
+
 typedef __attribute__((address_space(3))) const uint16_t lds_u16_t;
 
 // an LDS array element as an LDS-space pointer (constant offsets then fold into
@@ -1255,7 +1265,7 @@ __global__ void __launch_bounds__(dec_heads(D) * 64, 1) decode_bf16(const Plan p
             const int kk = q / CH, pc = q % CH;
             const int j = clamp_key(kt, kt + kk);
             const int hs = min(hh, n_heads_here - 1);   // heads past Hkv load a real head, never read
-            const size_t off = (((size_t)blk * a.hkv + hg * HW + hs) * kBlock + (j & 15)) * D + ((pc ^ swz<D>(kk)) << 3);
+            const size_t off = (((size_t)blk * a.hkv + hg * HW + hs) * kBlock + (j & 15)) * D + ((pc ^ dswz<D>(kk)) << 3);
             dma_lds16(kpool + off, &sg.k[(i * HW + wave) * 64 * 8]);
             dma_lds16(vpool + off, &sg.v[(i * HW + wave) * 64 * 8]);
         }
@@ -1274,7 +1284,7 @@ __global__ void __launch_bounds__(dec_heads(D) * 64, 1) decode_bf16(const Plan p
     int k_off[KD];
 #pragma unroll
     for (int kd = 0; kd < KD; ++kd)
-        k_off[kd] = wave * HSZ + c16 * D + ((model_chunk(a.chunk_map, kd * 4 + q4) ^ swz<D>(c16)) << 3);
+        k_off[kd] = wave * HSZ + c16 * D + ((model_chunk(a.chunk_map, kd * 4 + q4) ^ dswz<D>(c16)) << 3);
     constexpr int NTC = KD;   // NeoX: 2 chunks for each of the KD/2 steps; GPT-J: 1 for each of KD
     int t_off[NTC];
 #pragma unroll
@@ -1288,7 +1298,7 @@ __global__ void __launch_bounds__(dec_heads(D) * 64, 1) decode_bf16(const Plan p
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
             const int d = db * 16 + 4 * (lane & 3);
-            v_off[db] = wave * HSZ + key * D + (((d >> 3) ^ swz<D>(key)) << 3) + (d & 7);
+            v_off[db] = wave * HSZ + key * D + (((d >> 3) ^ dswz<D>(key)) << 3) + (d & 7);
         }
     }
 
