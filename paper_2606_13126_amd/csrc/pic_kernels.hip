@@ -658,16 +658,23 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
             dma_lds4(btab + blk, &mblk[t & 1][0]);
         }
     };
+    // every copy's row offset first (the block ids are LDS reads, and no read can pass
+    // a copy instruction, so reading them between copies would serialise one LDS
+    // round trip per copy), then the copies back to back
     auto issue_direct = [&](int t, int buf) {
         const int kt = kt0 + t * BN;
+        size_t row_off[DPW];
 #pragma unroll
         for (int i = 0; i < DPW; ++i) {
             const int jj = clamp_key(kt, kt + dkey(i));
             const int phys = mblk[t & 1][(jj - kt) >> 4];
-            const size_t row_off = (((size_t)phys * a.hkv + kvh) * kBlock + (jj & 15)) * D;
+            row_off[i] = (((size_t)phys * a.hkv + kvh) * kBlock + (jj & 15)) * D + dchunk(i) * 8;
+        }
+#pragma unroll
+        for (int i = 0; i < DPW; ++i) {
             const int lds_off = (DPW * wave_u + i) * 64 * 8;
-            dma_lds16(vpool + row_off + dchunk(i) * 8, &vs[buf][lds_off]);
-            if (!ROPE) dma_lds16(kpool + row_off + dchunk(i) * 8, &ks[buf][lds_off]);
+            dma_lds16(vpool + row_off[i], &vs[buf][lds_off]);
+            if (!ROPE) dma_lds16(kpool + row_off[i], &ks[buf][lds_off]);
         }
     };
     auto load_tile = [&](int t, TileRegs* rr) {
