@@ -420,6 +420,7 @@ struct TileRegs {
     u32x4_t k[2];
     u32x4_t cs[2];
     int32_t pos;
+    int32_t phys;
     bool ok;
 };
 
@@ -661,14 +662,27 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
     // every copy's row offset first (the block ids are LDS reads, and no read can pass
     // a copy instruction, so reading them between copies would serialise one LDS
     // round trip per copy), then the copies back to back
+    // A tile that lies wholly inside the window needs no clamping: a copy's row is
+    // then its block id times the block stride plus a per-lane constant.
+    const size_t blk_stride = (size_t)a.hkv * kBlock * D;
+    uint32_t lane_off[DPW];
+#pragma unroll
+    for (int i = 0; i < DPW; ++i) lane_off[i] = (uint32_t)((kvh * kBlock + (dkey(i) & 15)) * D + dchunk(i) * 8);
+    auto full_tile = [&](int kt) { return kt >= kv_lo && kt + BN <= kv_hi; };
     auto issue_direct = [&](int t, int buf) {
         const int kt = kt0 + t * BN;
         size_t row_off[DPW];
+        if (full_tile(kt)) {
 #pragma unroll
-        for (int i = 0; i < DPW; ++i) {
-            const int jj = clamp_key(kt, kt + dkey(i));
-            const int phys = mblk[t & 1][(jj - kt) >> 4];
-            row_off[i] = (((size_t)phys * a.hkv + kvh) * kBlock + (jj & 15)) * D + dchunk(i) * 8;
+            for (int i = 0; i < DPW; ++i)
+                row_off[i] = (size_t)(uint32_t)mblk[t & 1][dkey(i) >> 4] * blk_stride + lane_off[i];
+        } else {
+#pragma unroll
+            for (int i = 0; i < DPW; ++i) {
+                const int jj = clamp_key(kt, kt + dkey(i));
+                const int phys = mblk[t & 1][(jj - kt) >> 4];
+                row_off[i] = (((size_t)phys * a.hkv + kvh) * kBlock + (jj & 15)) * D + dchunk(i) * 8;
+            }
         }
 #pragma unroll
         for (int i = 0; i < DPW; ++i) {
@@ -677,6 +691,25 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
             if (!ROPE) dma_lds16(kpool + row_off[i], &ks[buf][lds_off]);
         }
     };
+    auto load_meta = [&](int t, TileRegs* rr) {
+        if (!stager) return;
+#pragma unroll
+        for (int u = 0; u < SU; ++u) {
+            TileRegs& r = rr[u];
+            const int kr = kk + u * KSTEP;
+            r.pos = mpos[t & 1][kr];
+            r.phys = mblk[t & 1][kr >> 4];
+        }
+    };
+    // this thread's two K chunks within its key's row of a block (tiles start on block
+    // boundaries and KSTEP is a multiple of the block size, so the row within the
+    // block is the same for every tile and every u)
+    uint32_t k_off2[2];
+    {
+        const uint32_t row = (uint32_t)((kvh * kBlock + (kk & 15)) * D);
+        k_off2[0] = row + (STYLE == kNeox ? model_chunk(a.chunk_map, sc) * 8 : sc * 16);
+        k_off2[1] = row + (STYLE == kNeox ? model_chunk(a.chunk_map, sc + CH / 2) * 8 : sc * 16 + 8);
+    }
     auto load_tile = [&](int t, TileRegs* rr) {
         if (!stager) return;
 #pragma unroll
@@ -685,18 +718,11 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
         const int kr = kk + u * KSTEP;
         const int j = kt0 + t * BN + kr;
         r.ok = j >= kv_lo && j < kv_hi;
-        r.pos = mpos[t & 1][kr];
         r.k[0] = r.k[1] = u32x4_t{0, 0, 0, 0};
         if (r.ok) {
-            const int phys = mblk[t & 1][kr >> 4];
-            const uint16_t* kp = kpool + (((size_t)phys * a.hkv + kvh) * kBlock + (j & 15)) * D;
-            if (STYLE == kNeox) {
-                r.k[0] = *reinterpret_cast<const u32x4_t*>(kp + model_chunk(a.chunk_map, sc) * 8);
-                r.k[1] = *reinterpret_cast<const u32x4_t*>(kp + model_chunk(a.chunk_map, sc + CH / 2) * 8);
-            } else {
-                r.k[0] = *reinterpret_cast<const u32x4_t*>(kp + sc * 16);
-                r.k[1] = *reinterpret_cast<const u32x4_t*>(kp + sc * 16 + 8);
-            }
+            const uint16_t* kp = kpool + (size_t)(uint32_t)r.phys * blk_stride;
+            r.k[0] = *reinterpret_cast<const u32x4_t*>(kp + k_off2[0]);
+            r.k[1] = *reinterpret_cast<const u32x4_t*>(kp + k_off2[1]);
             if (TABLE && (uint32_t)r.pos < (uint32_t)a.rope_len) {
                 const u32x4_t* tp = reinterpret_cast<const u32x4_t*>(reinterpret_cast<const uint32_t*>(a.rope_table) +
                                                                      (size_t)r.pos * HALF + sc * 8);
@@ -774,6 +800,7 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
     wait_vmem_n<KD>();
     barrier_keep_vmem();
     issue_direct(0, 0);
+    load_meta(0, regs);
     load_tile(0, regs);
     q_finish();
     store_tile(0, regs);
@@ -808,6 +835,8 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
         const bool more = t + 1 < n_tiles;
         // direct loads of the next tile (no registers) go out first; the rotated-K
         // register loads wait until the score tile is dead (after the softmax)
+        if (more) load_meta(t + 1, regs);
+        
         dma_meta(t + 2);   // into the slot tile t's metadata has left
         if (more) issue_direct(t + 1, buf ^ 1);
         if (wave_live) {
@@ -951,8 +980,9 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
         }
         *reinterpret_cast<u32x4_t*>(dst + c * 8) = v;
     }
-    if (is_split && hi == 0 && row_valid)
-        *reinterpret_cast<float2*>(a.part_ml + (slot * kTileRows + (row - row_lo)) * 2) = make_float2(m_run, lt);
+    if (is_split && hi == 0 && row_valid)   // the lane's row is row_lo + 32 wave + l32
+        *reinterpret_cast<float2*>(a.part_ml + (slot * kTileRows + (32 * wave_u + (int)(threadIdx.x & 31))) * 2) =
+            make_float2(m_run, lt);
 }
 
 // ---------------------------------------------------------------------------------
