@@ -747,11 +747,24 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
         const bool need_cs = r.ok && !(TABLE && (uint32_t)r.pos < (uint32_t)a.rope_len);
         if (!TABLE || __builtin_amdgcn_ballot_w64(need_cs) != 0) {
             if (need_cs) {
+                if (TABLE) {
+                    // rare: one compact loop, each new entry shifted in at the end of the
+                    // window, keeps the code inside the tile loop small
+#pragma unroll 1
+                    for (int k = 0; k < 8; ++k) {
+                        float c, sn;
+                        rope_cs(r.pos, fsteps[sc * 8 + k], c, sn);
 #pragma unroll
-                for (int k = 0; k < 8; ++k) {
-                    float c, sn;
-                    rope_cs(r.pos, fsteps[sc * 8 + k], c, sn);
-                    e[k] = bf16_entry(c, sn);
+                        for (int m = 0; m < 7; ++m) e[m] = e[m + 1];
+                        e[7] = bf16_entry(c, sn);
+                    }
+                } else {
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) {
+                        float c, sn;
+                        rope_cs(r.pos, fsteps[sc * 8 + k], c, sn);
+                        e[k] = bf16_entry(c, sn);
+                    }
                 }
             }
         }
@@ -1281,14 +1294,27 @@ __global__ void __launch_bounds__(dec_heads(D) * 64, 1) decode_bf16(const Plan p
                                   &sg.tab[(k * NT + wave * 64) * 4]);
                     if (!TABLE || __builtin_amdgcn_ballot_w64(!in_table) != 0) {
                         if (!in_table) {
-                            u32x4_t w;
+                            uint32_t w[4] = {0u, 0u, 0u, 0u};
+                            if (TABLE) {
+                                // rare with a table: a compact loop, entries shifted in
+#pragma unroll 1
+                                for (int e = 0; e < 4; ++e) {
+                                    float ce, se;
+                                    rope_cs(pos, fstep[4 * lc + e], ce, se);
+                                    w[0] = w[1];
+                                    w[1] = w[2];
+                                    w[2] = w[3];
+                                    w[3] = bf16_entry(ce, se);
+                                }
+                            } else {
 #pragma unroll
-                            for (int e = 0; e < 4; ++e) {
-                                float ce, se;
-                                rope_cs(pos, fstep[4 * lc + e], ce, se);
-                                w[e] = bf16_entry(ce, se);
+                                for (int e = 0; e < 4; ++e) {
+                                    float ce, se;
+                                    rope_cs(pos, fstep[4 * lc + e], ce, se);
+                                    w[e] = bf16_entry(ce, se);
+                                }
                             }
-                            *reinterpret_cast<u32x4_t*>(&sg.tab[c * 4]) = w;
+                            *reinterpret_cast<u32x4_t*>(&sg.tab[c * 4]) = u32x4_t{w[0], w[1], w[2], w[3]};
                         }
                     }
                 }
