@@ -617,6 +617,12 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
 #pragma unroll
     for (int db = 0; db < DB; ++db) acc[db] = f32x16_t{};
     float m_run = kNegBig, l_run = 0.f;
+    // The S^T chain starts from nbias = -m_run (0 while m_run is kNegBig, i.e. no
+    // visible key yet), so that it returns the scores relative to the reference
+    // maximum and the exponentials need no subtraction; `thr` is the shifted
+    // maximum above which the reference moves (8, or any score before the first).
+    f32x16_t nbias = f32x16_t{};
+    float thr = kNegBig;
 
     const int32_t* btab = a.block_tables + (size_t)g.req * a.max_blocks;
     const uint16_t* kpool = static_cast<const uint16_t*>(a.k_pool);
@@ -860,13 +866,11 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
             // MFMA chains interleaved (each accumulator was last written two MFMAs back)
             f32x16_t s[NH];
 #pragma unroll
-            for (int mb = 0; mb < NH; ++mb) s[mb] = f32x16_t{};
-#pragma unroll
             for (int kd = 0; kd < KD; ++kd)
 #pragma unroll
                 for (int mb = 0; mb < NH; ++mb) {
                     const bf16x8_t af = *reinterpret_cast<const bf16x8_t*>(kb + k_off[kd] + mb * 32 * D);
-                    s[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, qb[kd], s[mb], 0, 0, 0);
+                    s[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, qb[kd], kd == 0 ? nbias : s[mb], 0, 0, 0);
                 }
             // keep the K operand reads six reads ahead of their MFMAs (left alone, the
             // compiler waits on each read right after issuing it)
@@ -904,13 +908,22 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
 #pragma unroll
                 for (int j = 0; j < 16; ++j) mx = fmaxf(mx, s[mb][j]);
             mx = max_xor32(mx);
-            if (__builtin_amdgcn_ballot_w64(mx > m_run + 8.f) != 0) {
-                const float m_new = fmaxf(m_run, mx);
+            if (__builtin_amdgcn_ballot_w64(mx > thr) != 0) {
+                const float m_off = m_run > kNegBig ? m_run : 0.f;   // what the chain subtracted
+                const float m_new = fmaxf(m_run, mx + m_off);
                 const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
                 l_run *= alpha;
 #pragma unroll
                 for (int db = 0; db < DB; ++db) acc[db] *= alpha;
                 m_run = m_new;
+                const bool seen = m_new > kNegBig;
+                const float d = seen ? m_new - m_off : 0.f;
+#pragma unroll
+                for (int mb = 0; mb < NH; ++mb) s[mb] -= d;
+                const float nb = seen ? -m_new : 0.f;
+#pragma unroll
+                for (int j = 0; j < 16; ++j) nbias[j] = nb;
+                thr = seen ? 8.f : kNegBig;
             }
             // probabilities rounded to bf16 for P V; the row sum adds exactly those, two
             // at a time
@@ -923,8 +936,8 @@ __global__ void __launch_bounds__(kThreads, 512 / kThreads) prefill_bf16(const P
                     u32x4_t w;
 #pragma unroll
                     for (int m = 0; m < 4; ++m) {
-                        const float p0 = __builtin_amdgcn_exp2f(s[mb][8 * k2 + 2 * m] - m_run);
-                        const float p1 = __builtin_amdgcn_exp2f(s[mb][8 * k2 + 2 * m + 1] - m_run);
+                        const float p0 = __builtin_amdgcn_exp2f(s[mb][8 * k2 + 2 * m]);
+                        const float p1 = __builtin_amdgcn_exp2f(s[mb][8 * k2 + 2 * m + 1]);
                         w[m] = pack_bf16(p0, p1);
                         part[m & 1] = sum2_bf16(w[m], part[m & 1]);
                     }
