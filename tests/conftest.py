@@ -15,8 +15,8 @@ def pytest_configure(config):
 
 def pytest_terminal_summary(terminalreporter):
     """Print every GPU-vs-reference comparison of the run (max-abs, relative L2 and
-    the largest reference entry, which shows whether max-abs binds) and keep a copy
-    in gpurun_out/parity_summary.txt when that folder exists."""
+    the largest reference entry, which shows whether max-abs binds) and, when the
+    environment variable PIC_PARITY_SUMMARY names a file, write a copy there."""
     try:
         from tests.gpu_util import RECORDS
     except Exception:  # pragma: no cover
@@ -29,7 +29,7 @@ def pytest_terminal_summary(terminalreporter):
     terminalreporter.write_line("parity records (GPU vs oracle or vs another GPU path):")
     for ln in lines:
         terminalreporter.write_line(ln)
-    out = os.path.join(ROOT, "gpurun_out")
-    if os.path.isdir(out):
-        with open(os.path.join(out, "parity_summary.txt"), "w") as f:
+    out = os.environ.get("PIC_PARITY_SUMMARY")
+    if out:
+        with open(out, "w") as f:
             f.write("\n".join(lines) + "\n")
