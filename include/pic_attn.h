@@ -19,7 +19,8 @@
  *    ids or slots are undefined behaviour.
  *  - "DEVICE" pointers are HIP device memory; "HOST" pointers are host memory read
  *    during the call only.  All buffers are owned by the caller; the library
- *    allocates nothing and keeps no state between calls.
+ *    allocates nothing and keeps no state between calls (the one exception is the
+ *    per-GPU device scratch of pic_attn_decode_noalloc, described there).
  *  - Work is enqueued asynchronously on `stream` (a hipStream_t, or NULL for the
  *    null stream).  Kernel execution errors surface at the caller's next sync.
  *  - Tensors are dense and row-major in the shapes given.  Q, O, the K/V pools
