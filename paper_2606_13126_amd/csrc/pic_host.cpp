@@ -117,10 +117,16 @@ struct HostPlan {
     int64_t n_items = 0;       // blocks of the attention launch
     int64_t n_parts = 0;       // split partial slots
     int64_t n_merge = 0;       // blocks of the merge launch
-    bool dec_kernel = false;   // decode through the one-query kernel (bf16, G <= 16)
+    bool dec_kernel = false;   // decode through the one-query kernel (bf16, G <= kDecMaxG)
 };
 
 int32_t round_up(int64_t x, int64_t m) { return (int32_t)((x + m - 1) / m * m); }
+
+// Decode workgroups per (request, key split): KV heads in groups of dec_kv_per_wg.
+int64_t dec_head_groups(const pic_config* c) {
+    const int64_t per_wg = pic::dec_kv_per_wg(c->head_dim, c->num_q_heads / c->num_kv_heads);
+    return (c->num_kv_heads + per_wg - 1) / per_wg;
+}
 
 // Groups, their split policy and bases.  f32 groups hold one item per
 // (query token, query head); bf16 groups hold (row tile, KV head, split) items.
@@ -167,8 +173,7 @@ pic_status make_plan(const pic_config* c, const pic_batch_host* b, bool decode, 
         // Decode items are (request, key split, group of KV heads).  One workgroup
         // holds a CU, so cut the keys into chunks of about the average work per CU
         // (at least 4 cache blocks) and balance the splits of each request.
-        const int64_t hw = pic::dec_heads(c->head_dim);
-        const int64_t n_hg = (c->num_kv_heads + hw - 1) / hw;
+        const int64_t n_hg = dec_head_groups(c);
         int64_t tiles_total = 0;
         for (auto& g : hp.groups)
             tiles_total += n_hg * (((int64_t)g.tok0 + 1 - g.win + pic::kDecTileKeys - 1) / pic::kDecTileKeys);
@@ -220,10 +225,6 @@ pic_status make_plan(const pic_config* c, const pic_batch_host* b, bool decode, 
         });
     }
     return PIC_OK;
-}
-
-int64_t dec_head_groups(const pic_config* c) {
-    return (c->num_kv_heads + pic::dec_heads(c->head_dim) - 1) / pic::dec_heads(c->head_dim);
 }
 
 int64_t items_of(const pic_config* c, const HostPlan& hp, const pic::Group& g) {
@@ -635,7 +636,7 @@ pic_status pic_plan_debug(const pic_config* cfg, const pic_batch_host* batch, in
                     if (kl >= kh) continue;
                     for (int kvh = 0; kvh < cfg->num_kv_heads; ++kvh) {
                         const int32_t slot =
-                            g.n_split > 1 ? (int32_t)(g.part_base + s * n_hg + kvh / pic::dec_heads(cfg->head_dim)) : -1;
+                            g.n_split > 1 ? (int32_t)(g.part_base + s * n_hg + kvh / pic::dec_kv_per_wg(cfg->head_dim, G)) : -1;
                         emit(g.req, kvh, 0, G, kl, kh, g.tok0, slot);
                     }
                 }

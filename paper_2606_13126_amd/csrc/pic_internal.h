@@ -21,12 +21,17 @@ constexpr int kUploadGroups = 80; // groups carried by one plan-upload launch
 constexpr int kTargetCUs = 256;   // MI355X compute units the split policy fills
 constexpr int kMergeRows = 8;     // rows per block of the split merge
 constexpr int kDecTileKeys = 16;  // keys per decode tile (one cache block)
-constexpr int kDecMaxG = 16;      // query heads per KV head the decode kernel handles
+constexpr int kDecMaxG = 64;      // query heads per KV head the decode kernel handles
 #ifndef PIC_DEC_HEADS_D128
 #define PIC_DEC_HEADS_D128 8
 #endif
-// KV heads per decode workgroup (one wave each)
+// Waves of a decode workgroup (and K/V head slots of its LDS stages)
 constexpr int dec_heads(int head_dim) { return head_dim == 128 ? PIC_DEC_HEADS_D128 : 8; }
+// Waves per KV head in the decode kernel: each takes 16 of the KV head's query
+// heads (the columns of its 16x16 MFMA tiles)
+constexpr int dec_col_blocks(int group) { return group <= 16 ? 1 : group <= 32 ? 2 : 4; }
+// KV heads per decode workgroup
+constexpr int dec_kv_per_wg(int head_dim, int group) { return dec_heads(head_dim) / dec_col_blocks(group); }
 
 // One query span of one request (prefill) or one request's last token (decode).
 // Its work items are (row tile, KV head, key split) triples -- (key split, head

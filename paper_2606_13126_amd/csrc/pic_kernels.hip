@@ -1125,8 +1125,10 @@ struct Idx {
 // decode_bf16
 //
 // One query per (request, query head).  Workgroup = (request, key split, group of
-// HW KV heads); wave w owns KV head HW*hg + w and its G <= 16 query heads as the 16
-// columns of 16x16 MFMA tiles.  A tile is 16 keys = one cache block, so its K or V
+// HH = HW / CB KV heads): a KV head's G <= 64 query heads are split over CB =
+// ceil(G / 16) waves (1, 2 or 4), each holding 16 of them as the columns of its
+// 16x16 MFMA tiles; wave w owns KV head HH*hg + w / CB and query heads
+// 16 (w % CB) ..+15 of its group.  A tile is 16 keys = one cache block, so its K or V
 // for the group's heads is one contiguous run of the pool.  Every global read of
 // the key loop goes straight to LDS (K unrotated, V, the cos/sin rows of the
 // tile's 16 keys, the positions of a later tile), NST tiles deep, so the only wait
@@ -1181,20 +1183,22 @@ __global__ void __launch_bounds__(dec_heads(D) * 64, 1) decode_bf16(const Plan p
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int c16 = lane & 15, q4 = lane >> 4;   // MFMA column (query / key row) and row group
-    const int n_hg = (a.hkv + HW - 1) / HW;
+    const int G = a.group;
+    const int CB = dec_col_blocks(G), HH = HW / CB;   // waves per KV head, KV heads per workgroup
+    const int kv_slot = wave / CB, qc = (wave % CB) * 16 + c16;   // KV head slot, this lane's query column
+    const int n_hg = (a.hkv + HH - 1) / HH;
     const Group g = group_of<false>(plan, blockIdx.x);
     const int part_base = g.part_base;
     const int li = blockIdx.x - g.item_base;
     if (li >= g.n_split * n_hg) return;
     const int split = li / n_hg, hg = li - (li / n_hg) * n_hg;
-    const int G = a.group;
     const int L = g.tok0 + 1;                    // keys of the request (the query is its last token)
     const int kv_lo = g.win + split * g.split_keys;
     const int kv_hi = min(kv_lo + g.split_keys, L);
     if (kv_lo >= kv_hi) return;
-    const int kvh = hg * HW + wave;              // this wave's KV head
-    const bool head_live = kvh < a.hkv;
-    const int n_heads_here = min(HW, a.hkv - hg * HW);
+    const int kvh = hg * HH + kv_slot;           // this wave's KV head
+    const bool head_live = kvh < a.hkv && qc - c16 < G;   // the head exists and some column is a query
+    const int n_heads_here = min(HH, a.hkv - hg * HH);
 
     if (ROPE)
         for (int i = tid; i < HALF; i += NT) fstep[i] = a.fstep[i];
@@ -1224,8 +1228,8 @@ __global__ void __launch_bounds__(dec_heads(D) * 64, 1) decode_bf16(const Plan p
     // ---- queries: B operand of S^T = K Q^T, rotated at the last token's position
     bf16x8_t qb[KD];
     {
-        const bool qv = head_live && c16 < G;
-        const int qh = kvh * G + c16;
+        const bool qv = head_live && qc < G;
+        const int qh = kvh * G + qc;
         const uint16_t* qp = static_cast<const uint16_t*>(a.q) + ((size_t)g.q_row0 * a.hq + qh) * D;
         float xf[KD][8];
 #pragma unroll
@@ -1341,7 +1345,7 @@ __global__ void __launch_bounds__(dec_heads(D) * 64, 1) decode_bf16(const Plan p
             const int kk = q / CH, pc = q % CH;
             const int j = clamp_key(kt, kt + kk);
             const int hs = min(hh, n_heads_here - 1);   // heads past Hkv load a real head, never read
-            const size_t off = (((size_t)blk * a.hkv + hg * HW + hs) * kBlock + (j & 15)) * D + ((pc ^ dswz<D>(kk)) << 3);
+            const size_t off = (((size_t)blk * a.hkv + hg * HH + hs) * kBlock + (j & 15)) * D + ((pc ^ dswz<D>(kk)) << 3);
             dma_lds16(kpool + off, &sg.k[(i * HW + wave) * 64 * 8]);
             dma_lds16(vpool + off, &sg.v[(i * HW + wave) * 64 * 8]);
         }
@@ -1360,7 +1364,7 @@ __global__ void __launch_bounds__(dec_heads(D) * 64, 1) decode_bf16(const Plan p
     int k_off[KD];
 #pragma unroll
     for (int kd = 0; kd < KD; ++kd)
-        k_off[kd] = wave * HSZ + c16 * D + ((model_chunk(a.chunk_map, kd * 4 + q4) ^ dswz<D>(c16)) << 3);
+        k_off[kd] = kv_slot * HSZ + c16 * D + ((model_chunk(a.chunk_map, kd * 4 + q4) ^ dswz<D>(c16)) << 3);
     constexpr int NTC = KD;   // NeoX: 2 chunks for each of the KD/2 steps; GPT-J: 1 for each of KD
     int t_off[NTC];
 #pragma unroll
@@ -1374,7 +1378,7 @@ __global__ void __launch_bounds__(dec_heads(D) * 64, 1) decode_bf16(const Plan p
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
             const int d = db * 16 + 4 * (lane & 3);
-            v_off[db] = wave * HSZ + key * D + (((d >> 3) ^ dswz<D>(key)) << 3) + (d & 7);
+            v_off[db] = kv_slot * HSZ + key * D + (((d >> 3) ^ dswz<D>(key)) << 3) + (d & 7);
         }
     }
 
@@ -1483,8 +1487,8 @@ __global__ void __launch_bounds__(dec_heads(D) * 64, 1) decode_bf16(const Plan p
 
     // ---- epilogue: lane l holds query column l%16 and dims 16*db + 4*(l/16) + r
     const float lt = sum_xor32(sum_xor16(l_run));
-    if (!head_live || c16 >= G) return;
-    const int qh = kvh * G + c16;
+    if (!head_live || qc >= G) return;
+    const int qh = kvh * G + qc;
     if (g.n_split == 1) {
         const float inv = 1.f / lt;
         uint16_t* op = static_cast<uint16_t*>(a.o) + ((size_t)g.q_row0 * a.hq + qh) * D;
@@ -1513,14 +1517,17 @@ __global__ void __launch_bounds__(kMergeRows * D / 4) decode_merge(const Plan pl
     constexpr int TPR = D / 4;
     constexpr int HW = dec_heads(D);
     constexpr int U = 8;
-    const int n_hg = (a.hkv + HW - 1) / HW;
+    const int CB = dec_col_blocks(a.group), HH = HW / CB;
+    const int n_hg = (a.hkv + HH - 1) / HH;
     const Group g = group_of<true>(plan, blockIdx.x);
     if (g.n_split <= 1) return;
     const int qh = ((int)blockIdx.x - g.merge_base) * kMergeRows + (int)threadIdx.x / TPR;
     const int q4 = (int)threadIdx.x % TPR;
     if (qh >= a.hq) return;
     const int kvh = qh / a.group, c = qh - kvh * a.group;
-    const int hg = kvh / HW, prow = (kvh % HW) * 16 + c;
+    // the decode kernel's row of this query head: its wave (KV head slot x CB +
+    // column block) times 16 plus its column
+    const int hg = kvh / HH, prow = ((kvh % HH) * CB + c / 16) * 16 + c % 16;
     const int L = g.tok0 + 1;
     const int n_live = min(g.n_split, (L - g.win + g.split_keys - 1) / g.split_keys);   // non-empty splits
     float M = kNegBig, den = 0.f;

@@ -260,7 +260,11 @@ def test_rope_table_accuracy():
     (16, 16, 64, 1, 0),         # MHA, two head groups, computed cos/sin only
     (40, 10, 128, 0, 2000),     # G = 4, a partial second head group, table + computed
     (32, 2, 128, 1, None),      # G = 16, the widest query group of one MFMA tile
-    (34, 2, 64, 0, None),       # G = 17: the general kernel takes it
+    (34, 2, 64, 0, None),       # G = 17: two waves per KV head, the second with one query
+    (32, 1, 128, 0, None),      # G = 32 (MQA): two full column blocks
+    (48, 1, 64, 1, 0),          # G = 48: four waves per KV head, the last without queries
+    (128, 2, 128, 0, 2000),     # G = 64: four full column blocks, two KV heads per workgroup
+    (130, 2, 64, 0, None),      # G = 65: past the decode kernel, the prefill kernel takes it
 ])
 def test_decode_head_groups_and_windows(Hq, Hkv, D, style, table_len):
     wl = decode_case(Hq, Hkv, D, seed=20 + Hq)
@@ -341,7 +345,7 @@ def test_many_query_spans_prefill(dtype):
     check(wl, what=f"82 query spans {dtype}")
 
 
-@pytest.mark.parametrize("Hq,Hkv,D,style", [(32, 8, 128, 0), (34, 2, 64, 1)])
+@pytest.mark.parametrize("Hq,Hkv,D,style", [(32, 8, 128, 0), (34, 2, 64, 1), (32, 1, 128, 0)])
 def test_many_requests_decode(Hq, Hkv, D, style):
     wl = many_requests_decode(Hq=Hq, Hkv=Hkv, D=D)
     sh = shape_of(wl)
