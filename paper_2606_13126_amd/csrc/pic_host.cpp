@@ -124,7 +124,7 @@ int32_t round_up(int64_t x, int64_t m) { return (int32_t)((x + m - 1) / m * m); 
 
 // Decode workgroups per (request, key split): KV heads in groups of dec_kv_per_wg.
 int64_t dec_head_groups(const pic_config* c) {
-    const int64_t per_wg = pic::dec_kv_per_wg(c->head_dim, c->num_q_heads / c->num_kv_heads);
+    const int64_t per_wg = pic::dec_kv_per_wg(c->head_dim, c->num_kv_heads, c->num_q_heads / c->num_kv_heads);
     return (c->num_kv_heads + per_wg - 1) / per_wg;
 }
 
@@ -177,7 +177,8 @@ pic_status make_plan(const pic_config* c, const pic_batch_host* b, bool decode, 
         int64_t tiles_total = 0;
         for (auto& g : hp.groups)
             tiles_total += n_hg * (((int64_t)g.tok0 + 1 - g.win + pic::kDecTileKeys - 1) / pic::kDecTileKeys);
-        const int64_t chunk = std::max<int64_t>(4, (tiles_total + pic::kTargetCUs - 1) / pic::kTargetCUs);
+        const int64_t target = (int64_t)pic::kTargetCUs * pic::dec_wgs_per_cu(pic::dec_waves(c->head_dim, c->num_kv_heads, G));
+        const int64_t chunk = std::max<int64_t>(4, (tiles_total + target - 1) / target);
         for (auto& g : hp.groups) {
             const int64_t tiles = ((int64_t)g.tok0 + 1 - g.win + pic::kDecTileKeys - 1) / pic::kDecTileKeys;
             g.n_rt = 1;
@@ -636,7 +637,7 @@ pic_status pic_plan_debug(const pic_config* cfg, const pic_batch_host* batch, in
                     if (kl >= kh) continue;
                     for (int kvh = 0; kvh < cfg->num_kv_heads; ++kvh) {
                         const int32_t slot =
-                            g.n_split > 1 ? (int32_t)(g.part_base + s * n_hg + kvh / pic::dec_kv_per_wg(cfg->head_dim, G)) : -1;
+                            g.n_split > 1 ? (int32_t)(g.part_base + s * n_hg + kvh / pic::dec_kv_per_wg(cfg->head_dim, cfg->num_kv_heads, G)) : -1;
                         emit(g.req, kvh, 0, G, kl, kh, g.tok0, slot);
                     }
                 }

@@ -25,13 +25,23 @@ constexpr int kDecMaxG = 64;      // query heads per KV head the decode kernel h
 #ifndef PIC_DEC_HEADS_D128
 #define PIC_DEC_HEADS_D128 8
 #endif
-// Waves of a decode workgroup (and K/V head slots of its LDS stages)
+// Waves of a wide decode workgroup (and K/V head slots of its LDS stages)
 constexpr int dec_heads(int head_dim) { return head_dim == 128 ? PIC_DEC_HEADS_D128 : 8; }
 // Waves per KV head in the decode kernel: each takes 16 of the KV head's query
 // heads (the columns of its 16x16 MFMA tiles)
 constexpr int dec_col_blocks(int group) { return group <= 16 ? 1 : group <= 32 ? 2 : 4; }
+// Waves (and head slots) of a decode workgroup: 2 when the model's KV heads times
+// the waves each needs fit in 2 (one or two KV heads; three such workgroups share
+// a CU), else the wide workgroup
+constexpr int dec_waves(int head_dim, int hkv, int group) {
+    return hkv * dec_col_blocks(group) <= 2 ? 2 : dec_heads(head_dim);
+}
+// Decode workgroups of `waves` waves resident on one CU (LDS-bound)
+constexpr int dec_wgs_per_cu(int waves) { return waves == 2 ? 3 : 1; }
 // KV heads per decode workgroup
-constexpr int dec_kv_per_wg(int head_dim, int group) { return dec_heads(head_dim) / dec_col_blocks(group); }
+constexpr int dec_kv_per_wg(int head_dim, int hkv, int group) {
+    return dec_waves(head_dim, hkv, group) / dec_col_blocks(group);
+}
 
 // One query span of one request (prefill) or one request's last token (decode).
 // Its work items are (row tile, KV head, key split) triples -- (key split, head

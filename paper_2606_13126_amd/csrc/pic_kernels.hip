@@ -1097,22 +1097,22 @@ __device__ __forceinline__ float sum_xor16(float x) {
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-template <int D>
+template <int D, int HW>
 constexpr int dec_stages() {
-    // K + V of the workgroup's heads x 16 keys, plus the tile's cos/sin rows, per
-    // stage, within 144 KB of LDS
-    return 147456 / (2 * dec_heads(D) * kDecKeys * D * 2 + kDecKeys * D / 2 * 4) > 4
-               ? 4
-               : 147456 / (2 * dec_heads(D) * kDecKeys * D * 2 + kDecKeys * D / 2 * 4);
+    // K + V of the workgroup's HW heads x 16 keys, plus the tile's cos/sin rows, per
+    // stage, within the workgroup's share of 144 KB of LDS
+    constexpr int budget = 147456 / dec_wgs_per_cu(HW);
+    constexpr int stage = 2 * HW * kDecKeys * D * 2 + kDecKeys * D / 2 * 4;
+    return budget / stage > 4 ? 4 : budget / stage;
 }
 
 // One pipeline stage of the decode kernel in LDS.  Each stage is its own LDS
 // object (as is each stage's position slot) so that reading one stage does not
 // make the compiler wait for the global->LDS loads still filling another.
-template <int D, bool ROPE>
+template <int D, bool ROPE, int HW>
 struct DecStage {
-    uint16_t k[dec_heads(D) * kDecKeys * D];   // [head][key][D], chunks swizzled by key
-    uint16_t v[dec_heads(D) * kDecKeys * D];
+    uint16_t k[HW * kDecKeys * D];   // [head][key][D], chunks swizzled by key
+    uint16_t v[HW * kDecKeys * D];
     uint32_t tab[ROPE ? kDecKeys * D / 2 : 4];  // [key][pair] bf16 (c, s), 16-byte chunks swizzled by key
 };
 
@@ -1141,8 +1141,8 @@ struct Idx {
 // the B operand of the PV step, so probabilities never leave their lanes; row
 // statistics need two exchanges (lanes l^16 and l^32).
 // ---------------------------------------------------------------------------------
-template <int D, int STYLE, bool ROPE, bool TABLE>
-__global__ void __launch_bounds__(dec_heads(D) * 64, 1) decode_bf16(const Plan plan, const Args a) {
+template <int D, int STYLE, bool ROPE, bool TABLE, int HW>
+__global__ void __launch_bounds__(HW * 64, 1) decode_bf16(const Plan plan, const Args a) {
     typedef float f32x4_t __attribute__((ext_vector_type(4)));
     typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
     constexpr int KD = D / 32;             // 16x16x32 contraction steps of QK^T
@@ -1150,17 +1150,16 @@ __global__ void __launch_bounds__(dec_heads(D) * 64, 1) decode_bf16(const Plan p
     constexpr int CH = D / 8;              // 16-byte chunks per K/V row
     constexpr int HALF = D / 2;
     constexpr int TK = kDecKeys;
-    constexpr int HW = dec_heads(D);
     constexpr int NT = HW * 64;            // threads
     constexpr int HSZ = TK * D;            // elements of one head's tile
     constexpr int DPL = HW * HSZ / 8 / NT; // 16-byte direct loads per lane per tile, each of K and V
     constexpr int TROW = HALF / 4;         // 16-byte chunks (4 entries) per cos/sin row
     constexpr int TCH = TK * TROW;         // chunks of the tile's cos/sin rows
-    constexpr int NST = dec_stages<D>();   // pipeline stages (tiles resident in LDS)
+    constexpr int NST = dec_stages<D, HW>();   // pipeline stages (tiles resident in LDS)
     constexpr int LPS = 2 * DPL;           // unconditional loads per lane per stage
     static_assert(DPL >= 1 && TROW >= 8 && NST >= 2 && NST <= 4, "decode tile shape");
     static_assert((NST - 2) * LPS < 64, "vmcnt range");
-    typedef DecStage<D, ROPE> Stage;
+    typedef DecStage<D, ROPE, HW> Stage;
 
     __shared__ __attribute__((aligned(16))) Stage st0, st1, st2, st3;
     __shared__ int32_t pos0[TK], pos1[TK], pos2[TK], pos3[TK];
@@ -1512,10 +1511,9 @@ __global__ void __launch_bounds__(dec_heads(D) * 64, 1) decode_bf16(const Plan p
 // decode merge: one block per (request, kMergeRows query heads), one float4 of a
 // row per thread; the (max, sum) pairs and partial rows of up to 8 splits are
 // loaded together before they are combined (streaming log-sum-exp)
-template <int D>
+template <int D, int HW>
 __global__ void __launch_bounds__(kMergeRows * D / 4) decode_merge(const Plan plan, const Args a) {
     constexpr int TPR = D / 4;
-    constexpr int HW = dec_heads(D);
     constexpr int U = 8;
     const int CB = dec_col_blocks(a.group), HH = HW / CB;
     const int n_hg = (a.hkv + HH - 1) / HH;
@@ -1669,16 +1667,23 @@ hipError_t launch_attn_t(int dtype, const Plan& plan, const Args& a, hipStream_t
     return e;
 }
 
-template <int D, int STYLE, bool ROPE, bool TABLE>
-hipError_t launch_dec_t(const Plan& plan, const Args& a, hipStream_t st) {
-    hipLaunchKernelGGL((decode_bf16<D, STYLE, ROPE, TABLE>), dim3(plan.n_items), dim3(dec_heads(D) * 64), 0, st, plan, a);
+template <int D, int STYLE, bool ROPE, bool TABLE, int HW>
+hipError_t launch_dec_w(const Plan& plan, const Args& a, hipStream_t st) {
+    hipLaunchKernelGGL((decode_bf16<D, STYLE, ROPE, TABLE, HW>), dim3(plan.n_items), dim3(HW * 64), 0, st, plan, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (plan.n_merge > 0) {
-        hipLaunchKernelGGL((decode_merge<D>), dim3(plan.n_merge), dim3(kMergeRows * D / 4), 0, st, plan, a);
+        hipLaunchKernelGGL((decode_merge<D, HW>), dim3(plan.n_merge), dim3(kMergeRows * D / 4), 0, st, plan, a);
         e = hipGetLastError();
     }
     return e;
+}
+
+// the workgroup width the host plan assumed (dec_waves)
+template <int D, int STYLE, bool ROPE, bool TABLE>
+hipError_t launch_dec_t(const Plan& plan, const Args& a, hipStream_t st) {
+    if (dec_waves(D, a.hkv, a.group) == 2) return launch_dec_w<D, STYLE, ROPE, TABLE, 2>(plan, a, st);
+    return launch_dec_w<D, STYLE, ROPE, TABLE, dec_heads(D)>(plan, a, st);
 }
 
 template <int D, int STYLE>
