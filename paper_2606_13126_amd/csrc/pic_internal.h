@@ -30,14 +30,14 @@ constexpr int dec_heads(int head_dim) { return head_dim == 128 ? PIC_DEC_HEADS_D
 // Waves per KV head in the decode kernel: each takes 16 of the KV head's query
 // heads (the columns of its 16x16 MFMA tiles)
 constexpr int dec_col_blocks(int group) { return group <= 16 ? 1 : group <= 32 ? 2 : 4; }
-// Waves (and head slots) of a decode workgroup: 2 when the model's KV heads times
-// the waves each needs fit in 2 (one or two KV heads; three such workgroups share
-// a CU), else the wide workgroup
+// Waves (and head slots) of a decode workgroup: the model's KV heads times the
+// waves each needs, rounded up to 2 or 4 when that is at most 4 (three 2-wave or
+// two 4-wave workgroups share a CU), else the wide workgroup
 constexpr int dec_waves(int head_dim, int hkv, int group) {
-    return hkv * dec_col_blocks(group) <= 2 ? 2 : dec_heads(head_dim);
+    return hkv * dec_col_blocks(group) <= 2 ? 2 : hkv * dec_col_blocks(group) <= 4 ? 4 : dec_heads(head_dim);
 }
 // Decode workgroups of `waves` waves resident on one CU (LDS-bound)
-constexpr int dec_wgs_per_cu(int waves) { return waves == 2 ? 3 : 1; }
+constexpr int dec_wgs_per_cu(int waves) { return waves == 2 ? 3 : waves == 4 ? 2 : 1; }
 // KV heads per decode workgroup
 constexpr int dec_kv_per_wg(int head_dim, int hkv, int group) {
     return dec_waves(head_dim, hkv, group) / dec_col_blocks(group);

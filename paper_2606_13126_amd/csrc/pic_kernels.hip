@@ -1683,6 +1683,7 @@ hipError_t launch_dec_w(const Plan& plan, const Args& a, hipStream_t st) {
 template <int D, int STYLE, bool ROPE, bool TABLE>
 hipError_t launch_dec_t(const Plan& plan, const Args& a, hipStream_t st) {
     if (dec_waves(D, a.hkv, a.group) == 2) return launch_dec_w<D, STYLE, ROPE, TABLE, 2>(plan, a, st);
+    if (dec_waves(D, a.hkv, a.group) == 4) return launch_dec_w<D, STYLE, ROPE, TABLE, 4>(plan, a, st);
     return launch_dec_w<D, STYLE, ROPE, TABLE, dec_heads(D)>(plan, a, st);
 }
 

@@ -260,11 +260,13 @@ def test_rope_table_accuracy():
     (16, 16, 64, 1, 0),         # MHA, two head groups, computed cos/sin only
     (40, 10, 128, 0, 2000),     # G = 4, a partial second head group, table + computed
     (32, 2, 128, 1, None),      # G = 16, the widest query group of one MFMA tile (2-wave workgroups)
-    (34, 2, 64, 0, None),       # G = 17: two waves per KV head, the second with one query
+    (34, 2, 64, 0, None),       # G = 17: two waves per KV head, the second with one query (4-wave workgroups)
     (32, 1, 128, 0, None),      # G = 32 (MQA): two full column blocks, 2-wave workgroups
     (16, 1, 64, 1, 0),          # one KV head, G = 16: 2-wave workgroups, 4 stages, computed cos/sin
     (8, 1, 128, 0, 0),          # one KV head, G = 8: 2-wave workgroups, 2 stages, computed cos/sin
-    (48, 1, 64, 1, 0),          # G = 48: four waves per KV head, the last without queries
+    (28, 4, 128, 1, None),      # four KV heads, G = 7: 4-wave workgroups
+    (64, 1, 128, 0, 0),         # one KV head, G = 64: one 4-wave workgroup per head, computed cos/sin
+    (48, 1, 64, 1, 0),          # G = 48: four waves per KV head, the last without queries (4-wave workgroups)
     (128, 2, 128, 0, 2000),     # G = 64: four full column blocks, two KV heads per workgroup
     (130, 2, 64, 0, None),      # G = 65: past the decode kernel, the prefill kernel takes it
 ])
