@@ -1124,16 +1124,19 @@ struct Idx {
 // ---------------------------------------------------------------------------------
 // decode_bf16
 //
-// One query per (request, query head).  Workgroup = (request, key split, group of
-// HH = HW / CB KV heads): a KV head's G <= 64 query heads are split over CB =
-// ceil(G / 16) waves (1, 2 or 4), each holding 16 of them as the columns of its
-// 16x16 MFMA tiles; wave w owns KV head HH*hg + w / CB and query heads
-// 16 (w % CB) ..+15 of its group.  A tile is 16 keys = one cache block, so its K or V
+// One query per (request, query head).  Workgroup = HW waves (8, or 2 / 4 when
+// the model's KV heads need no more, dec_waves; narrower workgroups take a
+// matching share of the CU's LDS, so that several run side by side) = (request,
+// key split, group of HH = HW / CB KV heads): a KV head's G <= 64 query heads are
+// split over CB = ceil(G / 16) waves (1, 2 or 4), each holding 16 of them as the
+// columns of its 16x16 MFMA tiles; wave w owns KV head HH*hg + w / CB and query
+// heads 16 (w % CB) ..+15 of its group.  A tile is 16 keys = one cache block, so its K or V
 // for the group's heads is one contiguous run of the pool.  Every global read of
 // the key loop goes straight to LDS (K unrotated, V, the cos/sin rows of the
 // tile's 16 keys, the positions of a later tile), NST tiles deep, so the only wait
 // per tile is for the oldest stage.  Each wave rotates its own K operand in
-// registers right before the MFMA: every K element is consumed by exactly one wave.
+// registers right before the MFMA: with CB = 1 every K element is consumed by
+// exactly one wave (the CB waves of a wider query group each rotate it).
 //   S^T (16 keys x 16 queries) = K Q^T    v_mfma_f32_16x16x32_bf16
 //   O^T (16 dims x 16 queries) += V^T P^T v_mfma_f32_16x16x16_bf16, V^T through
 //                                          ds_read_b64_tr_b16
@@ -1679,7 +1682,7 @@ hipError_t launch_dec_w(const Plan& plan, const Args& a, hipStream_t st) {
     return e;
 }
 
-// the workgroup width the host plan assumed (dec_waves)
+// decode at the workgroup width the host plan assumed (dec_waves)
 template <int D, int STYLE, bool ROPE, bool TABLE>
 hipError_t launch_dec_t(const Plan& plan, const Args& a, hipStream_t st) {
     if (dec_waves(D, a.hkv, a.group) == 2) return launch_dec_w<D, STYLE, ROPE, TABLE, 2>(plan, a, st);
