@@ -62,3 +62,16 @@ def test_noalloc_decode_matches_workspace_decode_two_calls():
         assert_close(to_np(db.o), WO.run(wl), wl.dtype, f"noalloc {wl.name} vs oracle")
         del db
         torch.cuda.empty_cache()
+
+
+def test_noalloc_decode_narrow_workgroups():
+    # models with one or two KV heads decode with 2- and 4-wave workgroups (three or
+    # two per CU, more key splits): the scratch holds their partials too
+    for hq, hkv in ((32, 1), (64, 2)):
+        wl = many_requests_decode(num_reqs=64, Hq=hq, Hkv=hkv, D=128)
+        say(f"[gpu] noalloc decode Hq={hq} Hkv={hkv}: {wl.num_reqs} requests, {int(wl.seq_lens.sum())} keys")
+        db, ref = _case(wl)
+        assert torch.equal(db.o.view(torch.int16), ref.view(torch.int16)), (hq, hkv)
+        assert_close(to_np(db.o), WO.run(wl), wl.dtype, f"noalloc Hq={hq} Hkv={hkv} vs oracle")
+        del db
+        torch.cuda.empty_cache()
