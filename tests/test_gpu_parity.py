@@ -266,6 +266,8 @@ def test_rope_table_accuracy():
     (8, 1, 128, 0, 0),          # one KV head, G = 8: 2-wave workgroups, 2 stages, computed cos/sin
     (28, 4, 128, 1, None),      # four KV heads, G = 7: 4-wave workgroups
     (64, 1, 128, 0, 0),         # one KV head, G = 64: one 4-wave workgroup per head, computed cos/sin
+    (15, 3, 128, 0, None),      # three KV heads, G = 5: 4-wave workgroups with an idle head slot
+    (1, 1, 64, 1, None),        # one query head: a 2-wave workgroup with an idle head slot
     (48, 1, 64, 1, 0),          # G = 48: four waves per KV head, the last without queries (4-wave workgroups)
     (128, 2, 128, 0, 2000),     # G = 64: four full column blocks, two KV heads per workgroup
     (130, 2, 64, 0, None),      # G = 65: past the decode kernel, the prefill kernel takes it
