@@ -170,9 +170,10 @@ pic_status make_plan(const pic_config* c, const pic_batch_host* b, bool decode, 
 
     hp.dec_kernel = decode && c->dtype == PIC_BF16 && G <= pic::kDecMaxG;
     if (hp.dec_kernel) {
-        // Decode items are (request, key split, group of KV heads).  One workgroup
-        // holds a CU, so cut the keys into chunks of about the average work per CU
-        // (at least 4 cache blocks) and balance the splits of each request.
+        // Decode items are (request, key split, group of KV heads).  A wide workgroup
+        // holds a CU (narrow ones share it three or two ways), so cut the keys into
+        // chunks of about the average work per resident workgroup (at least 4 cache
+        // blocks) and balance the splits of each request.
         const int64_t n_hg = dec_head_groups(c);
         int64_t tiles_total = 0;
         for (auto& g : hp.groups)
