@@ -148,6 +148,21 @@ def test_shift_invariance_bf16():
     assert_close(base, ref, wl.dtype, "unshifted vs oracle")
 
 
+@pytest.mark.parametrize("Hq,Hkv", [(32, 1), (64, 2), (32, 8)])
+def test_decode_shift_invariance_full_size(Hq, Hkv):
+    # 64 requests x 8,193 keys through the 2-, 4- and 8-wave decode workgroups: adding
+    # a constant to every position leaves the scores unchanged (relative positions),
+    # so the outputs agree to bf16 rounding; checked where the fp64 oracle would be slow
+    reqs = [[Sp(8192, S, key=("d", r)), Sp(1, Pd, fresh=True)] for r in range(64)]
+    wl = W.build("decode_shift", reqs, num_q_heads=Hq, num_kv_heads=Hkv, head_dim=128, rope_theta=5e5,
+                 dtype=torch.bfloat16, seed=71, value_scale=0.5, num_blocks=64 * 514 + 16, decode=True, poison=False)
+    say(f"[gpu] decode shift invariance Hq={Hq} Hkv={Hkv}: {wl.num_reqs} requests x {int(wl.seq_lens[0])} keys")
+    base = to_np(gpu_run(wl).o)
+    wl.positions = (wl.positions.astype(np.int64) + 4321).astype(np.int32)
+    got = to_np(gpu_run(wl).o)
+    assert_close(got, base, wl.dtype, f"decode Hq={Hq} Hkv={Hkv} shift 4321 vs unshifted")
+
+
 @pytest.mark.parametrize("decode", [False, True])
 def test_positions_at_the_int32_limits(decode):
     # logical positions next to 2^31 - 1 and -2^31: the angle is an exact fixed-point
