@@ -89,6 +89,20 @@ def many_spans_prefill(dtype=torch.bfloat16, seed=60):
                         value_scale=0.5)
 
 
+def short_causal_spans_prefill(D=128, seed=62, cycles=24):
+    """Many short causal query spans, the shape of a prefill whose fresh documents are
+    short: fresh SSEP spans of 100, 64, 33, 160 and 7 tokens (4, 2, 2, 5 and 1 row
+    tiles of 8 heads, the last ones partial) in one request, 2,744 row-tile items
+    and 122 groups (the group table goes through the workspace); a second request
+    whose query span continues a cached span (window > 0); and a short PDEP tail
+    that sees every key (split)."""
+    lens = [100, 64, 33, 160, 7] * cycles
+    reqs = [[Sp(n, S | Q, fresh=True) for n in lens] + [Sp(16, Pd | Q, fresh=True)],
+            [Sp(64, S, key="pre"), Sp(48, S), Sp(37, Q, fresh=True)]]
+    return W.small_case(f"short_causal_spans_d{D}", reqs, Hq=64, Hkv=8, D=D, theta=5e5, dtype=torch.bfloat16,
+                        seed=seed, value_scale=0.5)
+
+
 def many_requests_decode(num_reqs=256, Hq=32, Hkv=8, D=128, seed=61):
     """256 decode requests of 1 to ~600 tokens (more groups than the kernel
     arguments hold; the longer ones are split, the shorter are not)."""

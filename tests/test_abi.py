@@ -292,6 +292,18 @@ def test_plan_exact_cover_many_spans(dtype):
     assert ws >= parts + 82 * 48 + 4 * (shape["attention_blocks"] + shape["merge_blocks"])
 
 
+def test_plan_exact_cover_short_causal_spans():
+    from tests.cases import short_causal_spans_prefill
+    wl = short_causal_spans_prefill()
+    n = check_exact_cover(wl, B.PIC_BF16, False)
+    assert n == wl.q.shape[0] * wl.num_q_heads
+    cfg = P.make_config(wl.num_q_heads, wl.num_kv_heads, wl.head_dim)
+    shape = P.pic_plan_shape(cfg, batch_of(wl), False)
+    assert shape["groups"] == 122 and shape["upload_launches"] == 2
+    # one attention block per (row tile, KV head, key split), padded to 8 per group
+    assert shape["attention_blocks"] >= len(P.pic_plan_debug(cfg, batch_of(wl), False)) == 2744
+
+
 @pytest.mark.parametrize("Hq,Hkv,D", [(32, 8, 128), (34, 2, 64)])
 def test_plan_exact_cover_many_requests_decode(Hq, Hkv, D):
     from tests.cases import many_requests_decode

@@ -7,7 +7,7 @@ import workloads as W
 from oracle import pic_oracle as O
 from oracle import workload_oracle as WO
 from tests.cases import (decode_case, many_requests_decode, many_spans_prefill, plant_rising_keys, rise_of_max,
-                         windows_decode_case, windows_prefill_case)
+                         short_causal_spans_prefill, windows_decode_case, windows_prefill_case)
 from tests.gpu_util import assert_close, gpu_run, say, to_np
 
 pytestmark = pytest.mark.gpu
@@ -364,6 +364,28 @@ def test_many_query_spans_prefill(dtype):
     if dtype == torch.bfloat16:
         assert sh["merge_blocks"] > 0
     check(wl, what=f"82 query spans {dtype}")
+
+
+@pytest.mark.parametrize("D", [128, 64])
+def test_short_causal_spans_prefill(D):
+    # 2,744 short causal row-tile items (ragged last row tiles, idle waves), a window
+    # > 0, 122 groups through the workspace table: RoPE from the table and computed,
+    # and the pre-rotated kernel with every position 0 (the rotation is the identity)
+    from paper_2606_13126_amd.runner import DeviceBatch
+    wl = short_causal_spans_prefill(D=D)
+    sh = shape_of(wl)
+    say(f"[gpu] short causal spans D={D}: {sh}")
+    assert sh["groups"] == 122
+    ref = WO.run(wl)
+    for table in (True, False):
+        assert_close(to_np(gpu_run(wl, table=table).o), ref, wl.dtype, f"short causal spans D={D} table={table}")
+    wl.positions = np.zeros_like(wl.positions)
+    ref0 = WO.run(wl)
+    ctl = DeviceBatch(wl, k_prerotated=True, table_positions=None)
+    ctl.write()
+    ctl.attend()
+    torch.cuda.synchronize()
+    assert_close(to_np(ctl.o), ref0, wl.dtype, f"short causal spans D={D} pre-rotated kernel, positions 0")
 
 
 @pytest.mark.parametrize("Hq,Hkv,D,style", [(32, 8, 128, 0), (34, 2, 64, 1), (32, 1, 128, 0)])
