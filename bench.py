@@ -339,7 +339,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-extra", action="store_true")
-    ap.add_argument("--workloads", default="llama3_70b_long,llama3_8b_rag,concurrent_reuse,decode_64req,"
+    ap.add_argument("--workloads", default="llama3_70b_long,llama3_70b_long_tail,llama3_70b_long_fresh,"
+                                           "llama3_8b_rag,concurrent_reuse,decode_64req,"
                                            "decode_64req_unshared,decode_256req_unshared",
                     help="extra workloads (names of workloads.WORKLOADS, decode_64req_unshared or "
                          "decode_256req_unshared)")

@@ -301,27 +301,37 @@ def decode_64req(seed: int = 1003, num_reqs: int = 64, num_spans: int = 16, span
                  num_blocks=nb, decode=True, poison=shared)
 
 
-def llama3_70b_long(seed: int = 1004, num_spans: int = 64, span_len: int = 512, tail: int = 512) -> Workload:
+def llama3_70b_long(seed: int = 1004, num_spans: int = 64, span_len: int = 512, tail: int = 512,
+                    part: str = "all") -> Workload:
     """Llama-3-70B-shaped long prefill: 64 SSEP spans of 512 tokens, a seeded half of
     them fresh (queried and written in the call), the other half cached, and a fresh
-    512-token PDEP query tail; 64/8 heads, head_dim 128, theta 5e5, bf16."""
+    512-token PDEP query tail; 64/8 heads, head_dim 128, theta 5e5, bf16.  ``part``
+    "tail" or "fresh" keeps the same spans and positions but queries only the tail
+    (the fresh spans are then cached) or only the fresh spans (the tail cached)."""
+    assert part in ("all", "tail", "fresh")
     rng = np.random.default_rng(seed + 7919)
     fresh = set(rng.choice(num_spans, size=num_spans // 2, replace=False).tolist())
     spans = []
     for i in range(num_spans):
-        if i in fresh:
+        if i in fresh and part != "tail":
             spans.append(Span(span_len, SSEP | QUERY, fresh=True))
         else:
             spans.append(Span(span_len, SSEP, key=("doc", i)))
-    spans.append(Span(tail, PDEP | QUERY, fresh=True))
+    if part == "fresh":
+        spans.append(Span(tail, PDEP, key=("tail",)))
+    else:
+        spans.append(Span(tail, PDEP | QUERY, fresh=True))
     L = num_spans * span_len + tail
     nb = L // BLOCK + 32
-    return build("llama3_70b_long_prefill", [spans], num_q_heads=64, num_kv_heads=8, head_dim=128,
+    name = "llama3_70b_long_prefill" + ("" if part == "all" else "_" + part)
+    return build(name, [spans], num_q_heads=64, num_kv_heads=8, head_dim=128,
                  rope_theta=5e5, dtype=torch.bfloat16, seed=seed, value_scale=0.5, num_blocks=nb)
 
 
 WORKLOADS = {"tiny_fp32": tiny_fp32, "llama3_8b_rag": llama3_8b_rag, "concurrent_reuse": concurrent_reuse,
-             "decode_64req": decode_64req, "llama3_70b_long": llama3_70b_long}
+             "decode_64req": decode_64req, "llama3_70b_long": llama3_70b_long,
+             "llama3_70b_long_tail": lambda **kw: llama3_70b_long(part="tail", **kw),
+             "llama3_70b_long_fresh": lambda **kw: llama3_70b_long(part="fresh", **kw)}
 
 
 def make(name: str, **kw) -> Workload:
