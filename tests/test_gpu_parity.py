@@ -6,8 +6,9 @@ import torch
 import workloads as W
 from oracle import pic_oracle as O
 from oracle import workload_oracle as WO
-from tests.cases import (decode_case, many_requests_decode, many_spans_prefill, plant_rising_keys, rise_of_max,
-                         short_causal_spans_prefill, windows_decode_case, windows_prefill_case)
+from tests.cases import (decode_case, long_context_decode, long_context_prefill, many_requests_decode,
+                         many_spans_prefill, plant_rising_keys, rise_of_max, short_causal_spans_prefill,
+                         windows_decode_case, windows_prefill_case)
 from tests.gpu_util import assert_close, gpu_run, say, to_np
 
 pytestmark = pytest.mark.gpu
@@ -386,6 +387,21 @@ def test_short_causal_spans_prefill(D):
     ctl.attend()
     torch.cuda.synchronize()
     assert_close(to_np(ctl.o), ref0, wl.dtype, f"short causal spans D={D} pre-rotated kernel, positions 0")
+
+
+@pytest.mark.parametrize("case", ["decode", "prefill"])
+def test_long_context(case):
+    # 131K-key contexts: decode of 2 requests holding 256 shared spans in their own
+    # orders, and a 40-token query tail over 131,072 cached keys (many key splits);
+    # RoPE from the table and computed.  (No peaked variant here: at these positions
+    # the planted keys' pair has turned by up to 0.3 rad, its rotated values are no
+    # longer exact in bf16, and scores of ~100 log2 units carry bf16 rounding errors
+    # of ~0.3 units, which the softmax turns into errors far past the tolerance.)
+    wl = long_context_decode() if case == "decode" else long_context_prefill()
+    say(f"[gpu] long context {case}: {int(wl.seq_lens.max())} keys, {shape_of(wl)}")
+    ref = WO.run(wl)
+    for table in (True, False):
+        assert_close(to_np(gpu_run(wl, table=table).o), ref, wl.dtype, f"long context {case} table={table}")
 
 
 @pytest.mark.parametrize("Hq,Hkv,D,style", [(32, 8, 128, 0), (34, 2, 64, 1), (32, 1, 128, 0)])
