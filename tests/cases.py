@@ -114,12 +114,12 @@ def long_context_decode(seed=81, num_reqs=2, num_spans=256, span_len=512):
                    dtype=torch.bfloat16, seed=seed, value_scale=0.5, num_blocks=nb, decode=True, poison=False)
 
 
-def long_context_prefill(seed=82, num_spans=256, span_len=512, tail=40):
+def long_context_prefill(seed=82, num_spans=256, span_len=512, tail=40, dtype=torch.bfloat16):
     """A 40-token PDEP query tail over 131,072 cached keys (256 SSEP spans)."""
     reqs = [[Sp(span_len, S, key=("d", i)) for i in range(num_spans)] + [Sp(tail, Pd | Q, fresh=True)]]
     nb = (num_spans * span_len + tail) // 16 + 16
     return W.build("long_context_prefill", reqs, num_q_heads=8, num_kv_heads=2, head_dim=128, rope_theta=5e5,
-                   dtype=torch.bfloat16, seed=seed, value_scale=0.5, num_blocks=nb, poison=False)
+                   dtype=dtype, seed=seed, value_scale=0.5, num_blocks=nb, poison=False)
 
 
 def many_requests_decode(num_reqs=256, Hq=32, Hkv=8, D=128, seed=61):

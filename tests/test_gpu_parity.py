@@ -389,7 +389,7 @@ def test_short_causal_spans_prefill(D):
     assert_close(to_np(ctl.o), ref0, wl.dtype, f"short causal spans D={D} pre-rotated kernel, positions 0")
 
 
-@pytest.mark.parametrize("case", ["decode", "prefill"])
+@pytest.mark.parametrize("case", ["decode", "decode_gptj", "prefill", "prefill_fp32"])
 def test_long_context(case):
     # 131K-key contexts: decode of 2 requests holding 256 shared spans in their own
     # orders, and a 40-token query tail over 131,072 cached keys (many key splits);
@@ -397,11 +397,16 @@ def test_long_context(case):
     # the planted keys' pair has turned by up to 0.3 rad, its rotated values are no
     # longer exact in bf16, and scores of ~100 log2 units carry bf16 rounding errors
     # of ~0.3 units, which the softmax turns into errors far past the tolerance.)
-    wl = long_context_decode() if case == "decode" else long_context_prefill()
+    if case.startswith("decode"):
+        wl = long_context_decode()
+    else:
+        wl = long_context_prefill(dtype=torch.float32 if case == "prefill_fp32" else torch.bfloat16)
+    style = 1 if case == "decode_gptj" else 0
     say(f"[gpu] long context {case}: {int(wl.seq_lens.max())} keys, {shape_of(wl)}")
-    ref = WO.run(wl)
+    ref = WO.run(wl, style="gptj" if style else "neox")
     for table in (True, False):
-        assert_close(to_np(gpu_run(wl, table=table).o), ref, wl.dtype, f"long context {case} table={table}")
+        assert_close(to_np(gpu_run(wl, rope_style=style, table=table).o), ref, wl.dtype,
+                     f"long context {case} table={table}")
 
 
 @pytest.mark.parametrize("Hq,Hkv,D,style", [(32, 8, 128, 0), (34, 2, 64, 1), (32, 1, 128, 0)])
